@@ -1,0 +1,76 @@
+"""Symmetric-key RLWE encryption / decryption over the RNS chain (CPU oracle; test infrastructure only).
+
+The paper's accelerator only ever sees ciphertexts; encryption and decryption
+run in the trusted CPU domain on either side of each accelerator linear call
+(sections 3.2 and 4.2; the decrypt-then-encrypt refresh ct' = Enc(Dec(ct)) of
+section 3.2).  Those steps are not on the accelerator path; they exist here to
+make valid encrypted inputs and to check outputs by decryption.  The paper
+writes public-key encryption; the ct x pt path is indifferent to how the RLWE
+ciphertext was made, so the symmetric form is used (reading):
+
+    ct = (c0, c1) = (-a*s + m + e, a)            per limb, in NTT form,
+
+with s ternary, e a rounded Gaussian (sigma = 3.2, |e| <= 19) and a uniform.
+Because the NTT is a bijection of Z_q^N, drawing a uniformly in NTT form is
+the same distribution as drawing it in coefficient form; the random draws are
+inputs (they come from the seeded generators, never from here).
+
+Decryption is m + e' = INTT(c0 + c1 (.) NTT(s)), lifted by CRT to centred
+integers.
+
+Parity: pinned (tests/test_oracle_rlwe.py) against the coefficient-domain
+definition -a*s + m + e with the schoolbook product at small N, and by
+round trips.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .ntt import intt, ntt
+from .params import centre, crt_lift
+
+
+def _residues(v, q: int) -> np.ndarray:
+    return np.array([int(x) % q for x in v], dtype=np.uint64)
+
+
+def encrypt(m, s, a_ntt, e, qs, psis, log_n: int) -> np.ndarray:
+    """m, s, e: integer coefficient vectors (N,); a_ntt: uniform residues (L, N).
+
+    Returns the ciphertext (2, L, N) in NTT form.
+    """
+    L = len(qs)
+    n = 1 << log_n
+    ct = np.empty((2, L, n), dtype=np.uint64)
+    me = [int(x) + int(y) for x, y in zip(m, e)]
+    for l, (q, ps) in enumerate(zip(qs, psis)):
+        qq = np.uint64(q)
+        s_hat = ntt(_residues(s, q), q, ps, log_n)
+        me_hat = ntt(_residues(me, q), q, ps, log_n)
+        a = np.asarray(a_ntt[l], dtype=np.uint64) % qq
+        ct[1, l] = a
+        ct[0, l] = (me_hat + qq - (a * s_hat) % qq) % qq
+    return ct
+
+
+def decrypt_residues(ct, s, qs, psis, log_n: int) -> np.ndarray:
+    """Coefficient residues (L', N) of c0 + c1*s for a ciphertext (2, L', N) in NTT form."""
+    L = ct.shape[1]
+    out = np.empty((L, 1 << log_n), dtype=np.uint64)
+    for l in range(L):
+        q, ps = qs[l], psis[l]
+        qq = np.uint64(q)
+        s_hat = ntt(_residues(s, q), q, ps, log_n)
+        v = (np.asarray(ct[0, l], dtype=np.uint64) + (np.asarray(ct[1, l], dtype=np.uint64) * s_hat) % qq) % qq
+        out[l] = intt(v, q, ps, log_n)
+    return out
+
+
+def decrypt(ct, s, qs, psis, log_n: int) -> list[int]:
+    """Centred integer coefficients of the decrypted plaintext (CRT over all limbs of ct)."""
+    L = ct.shape[1]
+    res = decrypt_residues(ct, s, qs, psis, log_n)
+    Q = 1
+    for q in qs[:L]:
+        Q *= q
+    return [centre(c, Q) for c in crt_lift(res, qs[:L])]
