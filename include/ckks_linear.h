@@ -1,0 +1,179 @@
+/*
+ * ckks_linear.h -- C ABI of the MI355X (gfx950) CKKS ciphertext x plaintext
+ * linear-layer library.
+ *
+ * The operation is the accelerator side of a hybrid TEE/FHE serving design:
+ * projection and FFN layers evaluated on encrypted activations with public
+ * plaintext weights (paper section 3.2 and the threat model of section 3.5),
+ * with weights either encoded once and kept resident or re-encoded per call
+ * (section 4.2; fallback encoding is 34.4% of Qwen3-0.6B decode in the cost
+ * breakdown table of section 6.1), over CKKS in R_Q = Z_Q[X]/(X^N+1) with RNS
+ * limbs, levels and rescaling (section 2.1).
+ *
+ * Data model (all device buffers are caller-owned; the library keeps no
+ * pointer to them after a call returns):
+ *   - residues are uint32 in [0, q_l); every output is fully reduced;
+ *   - a ciphertext is two polynomials (c0, c1), each stored as `limbs`
+ *     contiguous rows of N residues:  ct[count][2][limbs][N];
+ *   - polynomials handed to the transforms are poly[count][limbs][N];
+ *     row r of a batch uses modulus q_(r mod limbs);
+ *   - "NTT form" is the negacyclic NTT of section 2.1's ring, unscaled, in
+ *     bit-reversed order:  A[i] = sum_k a_k psi^((2 brv(i) + 1) k) mod q,
+ *     psi the smallest primitive 2N-th root of unity mod q;
+ *   - `limbs` (1..L of the context) selects q_0 .. q_(limbs-1); rescaling
+ *     drops q_(limbs-1).
+ *
+ * Moduli: unless given, q_0 > q_1 > ... are the L largest primes in
+ * (2^29, 2^30) with q = 1 mod 2N.
+ *
+ * Errors: every entry point returns CKKS_OK (0) or a negative status and
+ * never throws.  Argument errors are detected on the host before any launch.
+ * Kernels run asynchronously on `stream` (a hipStream_t; NULL = the default
+ * stream), so device-side faults surface at the caller's next synchronisation.
+ * ckks_last_error() returns a thread-local description of the last failure.
+ * Device pointers must be 16-byte aligned.  Entry points taking a context are
+ * safe to call concurrently on different streams; outputs must not alias
+ * inputs unless stated.
+ */
+#ifndef CKKS_LINEAR_H
+#define CKKS_LINEAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ckks_ctx ckks_ctx;
+
+enum ckks_status {
+  CKKS_OK = 0,
+  CKKS_E_INVALID_ARG = -1, /* bad shape, pointer, alignment or modulus          */
+  CKKS_E_UNSUPPORTED = -2, /* valid request this build does not implement      */
+  CKKS_E_HIP = -3,         /* a HIP runtime call or launch failed              */
+  CKKS_E_WORKSPACE = -4    /* workspace missing or smaller than required       */
+};
+
+/* Operations that take a workspace (see ckks_workspace_bytes). */
+enum ckks_op {
+  CKKS_OP_MAC_SCALAR = 1, /* a = d_out, b = d_in  */
+  CKKS_OP_RESCALE = 2,    /* a = count, b unused  */
+  CKKS_OP_ENCODE_POLY = 3 /* a = count, b unused  */
+};
+
+/* MAC kernel selection for ckks_linear_mac_scalar (ckks_ctx_set_mac_algo). */
+enum ckks_mac_algo {
+  CKKS_MAC_AUTO = 0, /* library choice (int8 MFMA digit split)               */
+  CKKS_MAC_VALU = 1, /* u32 x u32 -> u64 vector multiply-add                 */
+  CKKS_MAC_MFMA = 2  /* exact int8 digit-split contractions on matrix cores  */
+};
+
+/* Context: the RNS modulus chain of one ring degree and its device tables
+ * (twiddles with Shoup companions, rescale inverses, encode FFT tables).
+ * The paper keeps one CKKS context per projection shape (section 4.2); here
+ * one context serves every shape that shares (N, chain).
+ *   out        receives the new context (host pointer); unchanged on error.
+ *   log_n      log2 N, 10..16.
+ *   num_limbs  L, 1..16.
+ *   moduli     host array of L distinct primes in (2^29, 2^30), each = 1 mod
+ *              2N, or NULL for the default chain.  Checked: CKKS_E_INVALID_ARG.
+ *   device     HIP device ordinal the tables live on; all later calls with
+ *              this context must run on that device.
+ * Allocates device memory (the only entry point that does, with destroy
+ * freeing it). */
+int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs,
+                    const uint32_t* moduli, int device);
+int ckks_ctx_destroy(ckks_ctx* ctx);
+/* Host copies of the chain: moduli q_l and roots psi_l (length L each). */
+int ckks_ctx_moduli(const ckks_ctx* ctx, uint32_t* out);
+int ckks_ctx_roots(const ckks_ctx* ctx, uint32_t* out);
+int ckks_ctx_info(const ckks_ctx* ctx, uint32_t* log_n, uint32_t* num_limbs);
+/* Select the scalar-weight MAC kernel (ckks_mac_algo); applies to later calls. */
+int ckks_ctx_set_mac_algo(ckks_ctx* ctx, int algo);
+
+/* Forward / inverse negacyclic NTT (section 2.1 ring; definition above),
+ * in place on polys[count][limbs][N] (device).  The inverse includes N^-1.
+ * count == 0 is a no-op. */
+int ckks_ntt(const ckks_ctx* ctx, uint32_t* polys, uint32_t count, uint32_t limbs,
+             void* stream);
+int ckks_intt(const ckks_ctx* ctx, uint32_t* polys, uint32_t count, uint32_t limbs,
+              void* stream);
+
+/* Scalar weight encoding (weights as constant plaintexts, section 4.2's
+ * pre-encoded GPU-resident weights in the one-ciphertext-per-feature
+ * packing):  w_enc[j][i][l] = rint(w[j][i] * scale) mod q_l, rint rounding
+ * half to even.
+ *   w      device fp64 [d_out][d_in]; |w * scale| < 2^63 and finite.
+ *   w_enc  device uint32 [d_out][d_in][limbs]. */
+int ckks_linear_encode_scalar(const ckks_ctx* ctx, const double* w, uint32_t d_out,
+                              uint32_t d_in, uint32_t limbs, double scale,
+                              uint32_t* w_enc, void* stream);
+
+/* Full-polynomial encoding of real slot vectors (the per-call fallback
+ * encode of section 4.2): the inverse canonical embedding with slot j at
+ * exp(i pi 5^j / N), m_k = (2/N) Re sum_j z_j exp(-i pi 5^j k / N), then
+ * p_k = rint(scale * m_k), reduced mod each q_l and taken to NTT form.
+ *   slots  device fp64 [count][N/2] (real slot values).
+ *   pt     device uint32 [count][limbs][N], NTT form.
+ * Supported for log_n <= 15 (CKKS_E_UNSUPPORTED above).  The spectral
+ * transform runs in fp64, so a coefficient whose scaled value lies within
+ * about 1e-9 of a rounding tie may differ by one from an exact evaluation. */
+int ckks_linear_encode_poly(const ckks_ctx* ctx, const double* slots, uint32_t count,
+                            uint32_t limbs, double scale, uint32_t* pt, void* stream);
+
+/* ct x pt MAC with scalar weights (FHE_Linear of Algorithm 3 in the
+ * one-ciphertext-per-feature packing): for every output j, component c,
+ * limb l and NTT slot k
+ *     ct_out[j][c][l][k] = sum_i w_enc[j][i][l] * ct_in[i][c][l][k]  mod q_l.
+ *   w_enc    device uint32 [d_out][d_in][limbs], residues < q_l.
+ *   ct_in    device uint32 [d_in][2][limbs][N].
+ *   ct_out   device uint32 [d_out][2][limbs][N]; must not overlap ct_in/w_enc.
+ *   workspace / workspace_bytes: device scratch of at least
+ *            ckks_workspace_bytes(ctx, CKKS_OP_MAC_SCALAR, d_out, d_in, limbs)
+ *            bytes (may be 0 for the VALU kernel); else CKKS_E_WORKSPACE.
+ * d_out == 0 is a no-op; d_in == 0 writes zeros. */
+int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc,
+                           const uint32_t* ct_in, uint32_t* ct_out, uint32_t d_out,
+                           uint32_t d_in, uint32_t limbs, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/* ct x pt MAC with full-polynomial NTT-form weights (the fallback-encode
+ * path of section 4.2): slot-wise
+ *     ct_out[j][c][l][k] = sum_i pt[j][i][l][k] * ct_in[i][c][l][k]  mod q_l,
+ * i.e. a negacyclic product per pair in the coefficient domain.
+ *   pt      device uint32 [d_out][d_in][limbs][N] (NTT form).
+ *   ct_in   device uint32 [d_in][2][limbs][N];  ct_out [d_out][2][limbs][N]. */
+int ckks_linear_mac_poly(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* ct_in,
+                         uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
+                         void* stream);
+
+/* Rescale (section 2.1: divide by the last prime, drop one level), NTT form
+ * in and out.  Per polynomial, with C the CRT lift of the coefficients over
+ * q_0..q_(limbs-1):  out = NTT_l( round(C / q_(limbs-1)) mod q_l ), l < limbs-1,
+ * computed as (c_l - NTT_l([INTT(c_(limbs-1))]_centred mod q_l)) * q_(limbs-1)^-1.
+ *   ct_in   device uint32 [count][2][limbs][N], limbs >= 2.
+ *   ct_out  device uint32 [count][2][limbs-1][N]; must not overlap ct_in.
+ *   workspace: ckks_workspace_bytes(ctx, CKKS_OP_RESCALE, count, 0, limbs)
+ *           bytes (0 for log_n <= 15). */
+int ckks_rescale(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t* ct_out,
+                 uint32_t count, uint32_t limbs, void* workspace, size_t workspace_bytes,
+                 void* stream);
+
+/* Workspace size in bytes for `op` (ckks_op) with the given sizes; 0 when
+ * none is needed; (size_t)-1 for an invalid request. */
+size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b,
+                            uint32_t limbs);
+
+/* Scale after rescaling a ciphertext of scale `scale_in` at `limbs` limbs:
+ * scale_in / q_(limbs-1) (the caller carries the scale). */
+double ckks_rescaled_scale(const ckks_ctx* ctx, double scale_in, uint32_t limbs);
+
+/* Thread-local text of the last error ("" if none). */
+const char* ckks_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CKKS_LINEAR_H */

@@ -1,0 +1,123 @@
+// Vector-ALU modular MAC kernels (gfx950).
+//
+// Scalar weights: per limb a modular GEMM (d_out x d_in) . (d_in x 2N); each
+// thread owns one (component, NTT slot) column and kRows output rows, keeps
+// u64 accumulators fed by v_mad_u64_u32, and reduces every 15 products
+// (15 * 2^60 + 2^30 < 2^64).  Weights are wave-uniform (scalar loads).
+// Full-polynomial weights: slot-wise products streamed once from HBM; each
+// thread owns one (output, limb, slot) and both ciphertext components.
+#include "ckks_internal.hpp"
+
+namespace ckks {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kRows = 8;
+constexpr int kLazy = 15;
+
+__global__ __launch_bounds__(kThreads) void mac_scalar_valu_kernel(
+    Tables tb, const uint32_t* __restrict__ w_enc, const uint32_t* __restrict__ ct_in,
+    uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
+  const uint32_t n = tb.n;
+  const uint32_t col = blockIdx.x * kThreads + threadIdx.x;  // < 2N
+  const uint32_t c = col >> tb.log_n;
+  const uint32_t k = col & (n - 1);
+  const uint32_t l = blockIdx.z;
+  const uint32_t j0 = blockIdx.y * kRows;
+  const uint32_t q = tb.q[l];
+  const double qr = tb.q_recip[l];
+  const size_t in_stride = 2ull * limbs * n;
+  const uint32_t* x_ptr = ct_in + (static_cast<size_t>(c) * limbs + l) * n + k;
+  size_t w_row[kRows];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    const uint32_t j = min(j0 + r, d_out - 1);  // clamp: rows past d_out are computed, not stored
+    w_row[r] = static_cast<size_t>(j) * d_in * limbs + l;
+  }
+  uint64_t acc[kRows];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) acc[r] = 0;
+  uint32_t i = 0;
+  while (i < d_in) {
+    const uint32_t stop = min(d_in, i + kLazy);
+    for (; i < stop; ++i) {
+      const uint64_t x = x_ptr[i * in_stride];
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) acc[r] += x * w_enc[w_row[r] + static_cast<size_t>(i) * limbs];
+    }
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) acc[r] = reduce_u64(acc[r], q, qr);
+  }
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    const uint32_t j = j0 + r;
+    if (j < d_out)
+      ct_out[((static_cast<size_t>(j) * 2 + c) * limbs + l) * n + k] = static_cast<uint32_t>(acc[r]);
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void mac_poly_kernel(
+    Tables tb, const uint32_t* __restrict__ pt, const uint32_t* __restrict__ ct_in,
+    uint32_t* __restrict__ ct_out, uint32_t d_in, uint32_t limbs) {
+  const uint32_t n = tb.n;
+  const uint32_t blocks_per_row = n / kThreads;
+  // blockIdx.x = (j * limbs + l) * blocks_per_row + kb
+  const size_t jl = blockIdx.x / blocks_per_row;
+  const uint32_t k = (blockIdx.x % blocks_per_row) * kThreads + threadIdx.x;
+  const uint32_t l = static_cast<uint32_t>(jl % limbs);
+  const size_t j = jl / limbs;
+  const uint32_t q = tb.q[l];
+  const double qr = tb.q_recip[l];
+  const size_t ln = static_cast<size_t>(limbs) * n;
+  const uint32_t* p_ptr = pt + (j * d_in * limbs + l) * n + k;
+  const uint32_t* x_ptr = ct_in + static_cast<size_t>(l) * n + k;
+  uint64_t a0 = 0, a1 = 0;
+  uint32_t i = 0;
+  while (i < d_in) {
+    const uint32_t stop = min(d_in, i + kLazy);
+    for (; i < stop; ++i) {
+      const uint64_t p = p_ptr[i * ln];
+      a0 += p * x_ptr[(2ull * i) * ln];
+      a1 += p * x_ptr[(2ull * i + 1) * ln];
+    }
+    a0 = reduce_u64(a0, q, qr);
+    a1 = reduce_u64(a1, q, qr);
+  }
+  uint32_t* o = ct_out + (j * 2 * limbs + l) * n + k;
+  o[0] = static_cast<uint32_t>(a0);
+  o[ln] = static_cast<uint32_t>(a1);
+}
+
+__global__ __launch_bounds__(kThreads) void zero_kernel(uint32_t* p, size_t words) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x;
+  const size_t stride = static_cast<size_t>(gridDim.x) * kThreads;
+  for (size_t k = i; k < words; k += stride) p[k] = 0;
+}
+
+}  // namespace
+
+hipError_t launch_mac_scalar_valu(const Tables& t, const uint32_t* w_enc, const uint32_t* ct_in,
+                                  uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
+                                  hipStream_t s) {
+  dim3 grid(2 * t.n / kThreads, (d_out + kRows - 1) / kRows, limbs);
+  mac_scalar_valu_kernel<<<grid, kThreads, 0, s>>>(t, w_enc, ct_in, ct_out, d_out, d_in, limbs);
+  return hipGetLastError();
+}
+
+hipError_t launch_mac_poly(const Tables& t, const uint32_t* pt, const uint32_t* ct_in,
+                           uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
+                           hipStream_t s) {
+  const size_t grid = static_cast<size_t>(d_out) * limbs * (t.n / kThreads);
+  mac_poly_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, s>>>(t, pt, ct_in, ct_out, d_in, limbs);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(uint32_t* p, size_t words, hipStream_t s) {
+  if (words == 0) return hipSuccess;
+  size_t grid = (words + kThreads - 1) / kThreads;
+  if (grid > 65536) grid = 65536;
+  zero_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, s>>>(p, words);
+  return hipGetLastError();
+}
+
+}  // namespace ckks

@@ -1,0 +1,150 @@
+// Batched negacyclic NTT / INTT kernels (gfx950).
+//
+// N <= 2^15: one workgroup per polynomial row; the row is read from HBM once
+// in group-0 layout (coalesced), transformed through register groups and
+// padded-LDS exchanges (at most 132 KiB of LDS), and written once.
+// N = 2^16 (256 KiB per row, above the 160 KiB LDS): two passes over HBM,
+// a column pass over the top 6 index bits (64 residues per thread, twiddles
+// uniform across the workgroup) and a block pass over 1024-point blocks.
+#include "ntt_core.hpp"
+
+namespace ckks {
+namespace {
+
+template <int LOGN, bool INV>
+__global__ __launch_bounds__(WholePlan<LOGN>::P::T) void ntt_whole_kernel(Tables tb, uint32_t* rows,
+                                                                          uint32_t limbs) {
+  using P = typename WholePlan<LOGN>::P;
+  constexpr int LOGE = WholePlan<LOGN>::LOGE;
+  __shared__ uint32_t lds[P::lds_words];
+  const size_t r = blockIdx.x;
+  const uint32_t l = static_cast<uint32_t>(r % limbs);
+  const uint32_t t = threadIdx.x;
+  uint32_t* a = rows + r * P::B;
+  const uint32_t q = tb.q[l];
+  const size_t toff = static_cast<size_t>(l) << LOGN;
+  uint32_t v[P::E];
+  if constexpr (!INV) {
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<0>(t, j)];
+    fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + toff, tb.fwd_shoup + toff, q, lds);
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) a[P::template pos<P::NG - 1>(t, j)] = v[j];
+  } else {
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<P::NG - 1>(t, j)];
+    inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + toff, tb.inv_shoup + toff, q, lds);
+    const uint32_t ni = tb.ninv[l], nis = tb.ninv_shoup[l];
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) a[P::template pos<0>(t, j)] = mul_shoup(v[j], ni, nis, q);
+  }
+}
+
+// N = 2^16, top 6 bits: thread owns column c (low 10 bits) of one row.
+constexpr int kColLogE = 6;
+constexpr int kColThreads = 256;
+
+template <bool INV>
+__global__ __launch_bounds__(kColThreads) void ntt16_cols_kernel(Tables tb, uint32_t* rows,
+                                                                 uint32_t limbs) {
+  using P = Plan<16, kColLogE>;
+  constexpr int kColsPerRow = 1 << (16 - kColLogE);
+  const size_t r = blockIdx.x / (kColsPerRow / kColThreads);
+  const uint32_t c = (blockIdx.x % (kColsPerRow / kColThreads)) * kColThreads + threadIdx.x;
+  const uint32_t l = static_cast<uint32_t>(r % limbs);
+  uint32_t* a = rows + (r << 16);
+  const uint32_t q = tb.q[l];
+  const size_t toff = static_cast<size_t>(l) << 16;
+  uint32_t v[P::E];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<0>(c, j)];
+  if constexpr (!INV) {
+    fwd_group<16, 16, kColLogE, 0>(v, c, 0, tb.fwd + toff, tb.fwd_shoup + toff, q);
+  } else {
+    inv_group<16, 16, kColLogE, 0>(v, c, 0, tb.inv + toff, tb.inv_shoup + toff, q);
+    const uint32_t ni = tb.ninv[l], nis = tb.ninv_shoup[l];
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = mul_shoup(v[j], ni, nis, q);
+  }
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) a[P::template pos<0>(c, j)] = v[j];
+}
+
+// N = 2^16, low 10 bits: one 64-thread workgroup per 1024-point block.
+constexpr int kBlkLogB = 10;
+constexpr int kBlkLogE = 4;
+
+template <bool INV>
+__global__ __launch_bounds__(1 << (kBlkLogB - kBlkLogE)) void ntt16_blocks_kernel(Tables tb,
+                                                                                 uint32_t* rows,
+                                                                                 uint32_t limbs) {
+  using P = Plan<kBlkLogB, kBlkLogE>;
+  __shared__ uint32_t lds[P::lds_words];
+  constexpr int kBlocksPerRow = 1 << (16 - kBlkLogB);
+  const size_t r = blockIdx.x / kBlocksPerRow;
+  const uint32_t blk = blockIdx.x % kBlocksPerRow;
+  const uint32_t l = static_cast<uint32_t>(r % limbs);
+  const uint32_t t = threadIdx.x;
+  uint32_t* a = rows + (r << 16) + (static_cast<size_t>(blk) << kBlkLogB);
+  const uint32_t q = tb.q[l];
+  const size_t toff = static_cast<size_t>(l) << 16;
+  uint32_t v[P::E];
+  if constexpr (!INV) {
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<0>(t, j)];
+    fwd_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.fwd + toff, tb.fwd_shoup + toff, q, lds);
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) a[P::template pos<P::NG - 1>(t, j)] = v[j];
+  } else {
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<P::NG - 1>(t, j)];
+    inv_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.inv + toff, tb.inv_shoup + toff, q, lds);
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) a[P::template pos<0>(t, j)] = v[j];
+  }
+}
+
+template <int LOGN>
+hipError_t launch_whole(const Tables& t, uint32_t* rows, size_t count, uint32_t limbs, bool inv,
+                        hipStream_t s) {
+  using P = typename WholePlan<LOGN>::P;
+  if (inv)
+    ntt_whole_kernel<LOGN, true><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs);
+  else
+    ntt_whole_kernel<LOGN, false><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs);
+  return hipGetLastError();
+}
+
+hipError_t launch_ntt16(const Tables& t, uint32_t* rows, size_t count, uint32_t limbs, bool inv,
+                        hipStream_t s) {
+  const uint32_t col_grid = static_cast<uint32_t>(count * ((1 << (16 - kColLogE)) / kColThreads));
+  const uint32_t blk_grid = static_cast<uint32_t>(count * (1 << (16 - kBlkLogB)));
+  constexpr int blk_threads = 1 << (kBlkLogB - kBlkLogE);
+  if (!inv) {
+    ntt16_cols_kernel<false><<<col_grid, kColThreads, 0, s>>>(t, rows, limbs);
+    ntt16_blocks_kernel<false><<<blk_grid, blk_threads, 0, s>>>(t, rows, limbs);
+  } else {
+    ntt16_blocks_kernel<true><<<blk_grid, blk_threads, 0, s>>>(t, rows, limbs);
+    ntt16_cols_kernel<true><<<col_grid, kColThreads, 0, s>>>(t, rows, limbs);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ntt(const Tables& t, uint32_t* rows, size_t count_rows, uint32_t limbs,
+                      bool inverse, hipStream_t s) {
+  if (count_rows == 0) return hipSuccess;
+  switch (t.log_n) {
+    case 10: return launch_whole<10>(t, rows, count_rows, limbs, inverse, s);
+    case 11: return launch_whole<11>(t, rows, count_rows, limbs, inverse, s);
+    case 12: return launch_whole<12>(t, rows, count_rows, limbs, inverse, s);
+    case 13: return launch_whole<13>(t, rows, count_rows, limbs, inverse, s);
+    case 14: return launch_whole<14>(t, rows, count_rows, limbs, inverse, s);
+    case 15: return launch_whole<15>(t, rows, count_rows, limbs, inverse, s);
+    case 16: return launch_ntt16(t, rows, count_rows, limbs, inverse, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace ckks

@@ -1,0 +1,149 @@
+// Register-group negacyclic NTT building blocks for gfx950.
+//
+// Transform (ring of section 2.1, NTT form as declared in ckks_linear.h):
+// merged-twiddle Cooley-Tukey (forward) and Gentleman-Sande (inverse), stage
+// s = 0..log N - 1 pairing index bits b = log N - 1 - s, twiddle index
+// 2^s + (x >> (b + 1)) into the bit-reversed power tables.
+//
+// A transform (or a 2^LOGB-point block of one) is split into groups of LOGE
+// consecutive index bits.  For one group a thread owns E = 2^LOGE residues
+// whose indices differ only in the group's window of bits, and runs all the
+// group's stages in registers (a radix-E butterfly network).  Between groups
+// the residues are exchanged through LDS, padded by one word per 32 so that
+// power-of-two strides spread across banks.  Group 0 covers the top bits, so
+// its window is a stride-T pattern (coalesced HBM access) and the last group's
+// window is contiguous per thread.
+#pragma once
+
+#include "ckks_internal.hpp"
+
+namespace ckks {
+
+__device__ __forceinline__ uint32_t lds_pad(uint32_t x) { return x + (x >> 5); }
+
+template <int LOGB, int LOGE>
+struct Plan {
+  static constexpr int B = 1 << LOGB;
+  static constexpr int LOGT = LOGB - LOGE;
+  static constexpr int T = 1 << LOGT;
+  static constexpr int E = 1 << LOGE;
+  static constexpr int NG = (LOGB + LOGE - 1) / LOGE;
+  static constexpr int lds_words = B + (B >> 5);
+  static constexpr int hi(int g) { return LOGB - 1 - g * LOGE; }
+  static constexpr int lo(int g) { return LOGB - (g + 1) * LOGE > 0 ? LOGB - (g + 1) * LOGE : 0; }
+  // Index (within the block) of element j of thread t in group g's layout.
+  template <int G>
+  static __device__ __forceinline__ uint32_t pos(uint32_t t, uint32_t j) {
+    constexpr int w = lo(G);
+    return (t & ((1u << w) - 1u)) | (j << w) | ((t >> w) << (w + LOGE));
+  }
+};
+
+// Forward stages of group G (bits hi..lo, descending).  LOGN is the full
+// transform size (for the stage number); blk is the block index above the
+// block's LOGB bits (0 for a whole-polynomial block).
+template <int LOGN, int LOGB, int LOGE, int G>
+__device__ __forceinline__ void fwd_group(uint32_t (&v)[1 << LOGE], uint32_t t, uint32_t blk,
+                                          const uint32_t* __restrict__ tw,
+                                          const uint32_t* __restrict__ tws, uint32_t q) {
+  using P = Plan<LOGB, LOGE>;
+  constexpr int w = P::lo(G);
+#pragma unroll
+  for (int b = P::hi(G); b >= P::lo(G); --b) {
+    const int s = LOGN - 1 - b;
+    const int lb = b - w;
+    const uint32_t base = (1u << s) + (blk << (LOGB - 1 - b)) +
+                          ((t >> w) << (w + LOGE - b - 1));
+#pragma unroll
+    for (int u = 0; u < (P::E >> (lb + 1)); ++u) {
+      const uint32_t idx = base + u;
+      const uint32_t wv = tw[idx], wsv = tws[idx];
+#pragma unroll
+      for (int low = 0; low < (1 << lb); ++low) {
+        const int j0 = (u << (lb + 1)) | low;
+        const int j1 = j0 | (1 << lb);
+        const uint32_t U = v[j0];
+        const uint32_t V = mul_shoup(v[j1], wv, wsv, q);
+        v[j0] = add_mod(U, V, q);
+        v[j1] = sub_mod(U, V, q);
+      }
+    }
+  }
+}
+
+// Inverse stages of group G (bits lo..hi, ascending).
+template <int LOGN, int LOGB, int LOGE, int G>
+__device__ __forceinline__ void inv_group(uint32_t (&v)[1 << LOGE], uint32_t t, uint32_t blk,
+                                          const uint32_t* __restrict__ tw,
+                                          const uint32_t* __restrict__ tws, uint32_t q) {
+  using P = Plan<LOGB, LOGE>;
+  constexpr int w = P::lo(G);
+#pragma unroll
+  for (int b = P::lo(G); b <= P::hi(G); ++b) {
+    const int s = LOGN - 1 - b;
+    const int lb = b - w;
+    const uint32_t base = (1u << s) + (blk << (LOGB - 1 - b)) +
+                          ((t >> w) << (w + LOGE - b - 1));
+#pragma unroll
+    for (int u = 0; u < (P::E >> (lb + 1)); ++u) {
+      const uint32_t idx = base + u;
+      const uint32_t wv = tw[idx], wsv = tws[idx];
+#pragma unroll
+      for (int low = 0; low < (1 << lb); ++low) {
+        const int j0 = (u << (lb + 1)) | low;
+        const int j1 = j0 | (1 << lb);
+        const uint32_t U = v[j0];
+        const uint32_t V = v[j1];
+        v[j0] = add_mod(U, V, q);
+        v[j1] = mul_shoup(sub_mod(U, V, q), wv, wsv, q);
+      }
+    }
+  }
+}
+
+// Move the thread's residues from group GF's layout to group GT's through LDS.
+template <int LOGB, int LOGE, int GF, int GT>
+__device__ __forceinline__ void exchange(uint32_t (&v)[1 << LOGE], uint32_t t, uint32_t* lds) {
+  using P = Plan<LOGB, LOGE>;
+  __syncthreads();  // earlier readers of lds are done
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) lds[lds_pad(P::template pos<GF>(t, j))] = v[j];
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) v[j] = lds[lds_pad(P::template pos<GT>(t, j))];
+}
+
+// Forward transform of one block held in registers in group-0 layout; on
+// return the registers hold group NG-1 layout.
+template <int LOGN, int LOGB, int LOGE, int G = 0>
+__device__ __forceinline__ void fwd_block(uint32_t (&v)[1 << LOGE], uint32_t t, uint32_t blk,
+                                          const uint32_t* __restrict__ tw,
+                                          const uint32_t* __restrict__ tws, uint32_t q,
+                                          uint32_t* lds) {
+  using P = Plan<LOGB, LOGE>;
+  if constexpr (G > 0) exchange<LOGB, LOGE, G - 1, G>(v, t, lds);
+  fwd_group<LOGN, LOGB, LOGE, G>(v, t, blk, tw, tws, q);
+  if constexpr (G + 1 < P::NG) fwd_block<LOGN, LOGB, LOGE, G + 1>(v, t, blk, tw, tws, q, lds);
+}
+
+// Inverse transform (without the N^-1 factor) of one block held in group
+// NG-1 layout; on return the registers hold group-0 layout.
+template <int LOGN, int LOGB, int LOGE, int G = Plan<LOGB, LOGE>::NG - 1>
+__device__ __forceinline__ void inv_block(uint32_t (&v)[1 << LOGE], uint32_t t, uint32_t blk,
+                                          const uint32_t* __restrict__ tw,
+                                          const uint32_t* __restrict__ tws, uint32_t q,
+                                          uint32_t* lds) {
+  using P = Plan<LOGB, LOGE>;
+  if constexpr (G < P::NG - 1) exchange<LOGB, LOGE, G + 1, G>(v, t, lds);
+  inv_group<LOGN, LOGB, LOGE, G>(v, t, blk, tw, tws, q);
+  if constexpr (G > 0) inv_block<LOGN, LOGB, LOGE, G - 1>(v, t, blk, tw, tws, q, lds);
+}
+
+// Per-N choice of residues per thread for whole-polynomial blocks.
+template <int LOGN>
+struct WholePlan {
+  static constexpr int LOGE = LOGN <= 12 ? 4 : 5;
+  using P = Plan<LOGN, LOGE>;
+};
+
+}  // namespace ckks

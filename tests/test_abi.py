@@ -1,0 +1,55 @@
+"""CPU-side checks of the C ABI: the library loads, every entry point that
+include/ckks_linear.h declares is exported and bound, and host-side argument
+errors come back as status codes (no GPU needed, no compute launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ckks_linear.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ckks_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for must in ("ckks_ntt", "ckks_intt", "ckks_linear_encode_scalar", "ckks_linear_encode_poly",
+                 "ckks_linear_mac_scalar", "ckks_linear_mac_poly", "ckks_rescale"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2606_17421_amd as ck
+    lib = ctypes.CDLL(ck.LIB_PATH)
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_declared()) == set(ck.EXPORTS)
+
+
+def test_null_context_is_rejected_without_a_gpu():
+    import paper_2606_17421_amd as ck
+    lib = ck._lib
+    assert lib.ckks_ntt(None, None, 1, 1, None) == ck.CKKS_E_INVALID_ARG
+    assert "null context" in ck.ckks_last_error()
+    assert lib.ckks_rescale(None, None, None, 1, 2, None, 0, None) == ck.CKKS_E_INVALID_ARG
+    assert lib.ckks_workspace_bytes(None, ck.CKKS_OP_RESCALE, 1, 0, 2) == ctypes.c_size_t(-1).value
+    h = ctypes.c_void_p()
+    assert lib.ckks_ctx_create(ctypes.byref(h), 9, 2, None, 0) == ck.CKKS_E_INVALID_ARG      # log_n < 10
+    assert lib.ckks_ctx_create(ctypes.byref(h), 14, 17, None, 0) == ck.CKKS_E_INVALID_ARG    # too many limbs
+    assert lib.ckks_ctx_create(None, 14, 2, None, 0) == ck.CKKS_E_INVALID_ARG
+    assert lib.ckks_ctx_destroy(None) == ck.CKKS_OK
+
+
+def test_product_path_does_not_touch_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2606_17421_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".hpp", ".h")):
+                src = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"\boracle\b", src.replace("the oracle", "")), f
