@@ -468,12 +468,15 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc, const uin
     e = ckks::launch_zero(ct_out, static_cast<size_t>(d_out) * 2 * limbs * ctx->n, s);
     return e == hipSuccess ? ok() : hip_fail(e, "zero launch");
   }
-  const bool use_mfma = ctx->mac_algo == CKKS_MAC_MFMA;
+  const bool mfma_ok = ckks::mac_mfma_supported(d_in);
+  if (ctx->mac_algo == CKKS_MAC_MFMA && !mfma_ok)
+    return fail(CKKS_E_UNSUPPORTED, "matrix-core MAC needs d_in <= 16384 (got %u)", d_in);
+  const bool use_mfma = ctx->mac_algo == CKKS_MAC_MFMA || (ctx->mac_algo == CKKS_MAC_AUTO && mfma_ok);
   if (use_mfma) {
     const size_t need = ckks::mac_mfma_workspace_bytes(d_out, d_in, limbs);
-    if (need && (!workspace || workspace_bytes < need))
+    if (!workspace || workspace_bytes < need)
       return fail(CKKS_E_WORKSPACE, "MAC workspace %zu bytes < %zu required", workspace_bytes, need);
-    if (need && !aligned16(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 16-byte aligned");
+    if (!aligned16(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 16-byte aligned");
     e = ckks::launch_mac_scalar_mfma(ctx->t, w_enc, ct_in, ct_out, d_out, d_in, limbs, workspace, s);
   } else {
     e = ckks::launch_mac_scalar_valu(ctx->t, w_enc, ct_in, ct_out, d_out, d_in, limbs, s);
@@ -523,7 +526,7 @@ size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b,
   if (!ctx || limbs < 1 || limbs > ctx->L) return static_cast<size_t>(-1);
   switch (op) {
     case CKKS_OP_MAC_SCALAR:
-      return ckks::mac_mfma_workspace_bytes(a, b, limbs);
+      return ctx->mac_algo == CKKS_MAC_VALU ? 0 : ckks::mac_mfma_workspace_bytes(a, b, limbs);
     case CKKS_OP_RESCALE:
       return limbs < 2 ? static_cast<size_t>(-1) : ckks::rescale_workspace_bytes(ctx->t, a);
     case CKKS_OP_ENCODE_POLY:

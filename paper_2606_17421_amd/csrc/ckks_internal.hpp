@@ -103,6 +103,7 @@ hipError_t launch_mac_scalar_valu(const Tables& t, const uint32_t* w_enc, const 
                                   hipStream_t s);
 
 size_t mac_mfma_workspace_bytes(uint32_t d_out, uint32_t d_in, uint32_t limbs);
+bool mac_mfma_supported(uint32_t d_in);
 hipError_t launch_mac_scalar_mfma(const Tables& t, const uint32_t* w_enc, const uint32_t* ct_in,
                                   uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
                                   void* workspace, hipStream_t s);
