@@ -96,16 +96,22 @@ def encode_poly(z, delta: float, qs, psis, log_n: int) -> np.ndarray:
 
 
 def decode(m, delta: float, log_n: int) -> np.ndarray:
-    """Slots z_j = (1/Delta) sum_k m_k zeta_j^k for integer (or real) coefficients m (N,)."""
+    """Slots z_j = (1/Delta) sum_k m_k zeta_j^k for integer (or real) coefficients m.
+
+    m is one coefficient vector (N,) or a batch (B, N); returns (N/2,) or (B, N/2).
+    """
     n = 1 << log_n
-    mf = np.array([float(x) for x in m], dtype=np.float64)
+    single = np.ndim(m) == 1 if not isinstance(m, list) else not isinstance(m[0], (list, np.ndarray))
+    rows = [m] if single else list(m)
+    mf = np.array([[float(x) for x in row] for row in rows], dtype=np.float64).T      # (N, B)
     cos_t, sin_t = _trig_tables(log_n)
     e = slot_exponents(log_n)
     k = np.arange(n, dtype=np.int64)
-    out = np.empty(n // 2, dtype=np.complex128)
+    out = np.empty((n // 2, mf.shape[1]), dtype=np.complex128)
     chunk = max(1, (1 << 22) // n)
     for j0 in range(0, n // 2, chunk):
         ej = e[j0:j0 + chunk]
         t = np.outer(ej, k) % (2 * n)
         out[j0:j0 + len(ej)] = (cos_t[t] @ mf + 1j * (sin_t[t] @ mf)) / delta
-    return out
+    out = out.T
+    return out[0] if single else out

@@ -22,22 +22,30 @@ All arrays are numpy uint64 with residues in [0, q); products stay < 2^60.
 """
 from __future__ import annotations
 
+from functools import lru_cache
+
 import numpy as np
 
 from .params import brv
 
 
+@lru_cache(maxsize=256)
 def _pow_table(base: int, count: int, q: int) -> np.ndarray:
+    """base^e mod q for e < count (cached, read-only)."""
     out = np.empty(count, dtype=np.uint64)
     x = 1
     for e in range(count):
         out[e] = x
         x = x * base % q
+    out.flags.writeable = False
     return out
 
 
+@lru_cache(maxsize=32)
 def brv_perm(log_n: int) -> np.ndarray:
-    return np.array([brv(i, log_n) for i in range(1 << log_n)], dtype=np.int64)
+    out = np.array([brv(i, log_n) for i in range(1 << log_n)], dtype=np.int64)
+    out.flags.writeable = False
+    return out
 
 
 def ntt_direct(a, q: int, psi: int, log_n: int, points=None) -> np.ndarray:

@@ -31,26 +31,34 @@ from .params import centre, crt_lift
 
 
 def _residues(v, q: int) -> np.ndarray:
-    return np.array([int(x) % q for x in v], dtype=np.uint64)
+    """Integer vector(s) (any shape, Python ints or int64) -> residues mod q (uint64)."""
+    v = np.asarray(v)
+    if v.dtype == object:
+        return np.vectorize(lambda x: int(x) % q, otypes=[np.uint64])(v)
+    return np.mod(v.astype(np.int64), q).astype(np.uint64)
 
 
 def encrypt(m, s, a_ntt, e, qs, psis, log_n: int) -> np.ndarray:
-    """m, s, e: integer coefficient vectors (N,); a_ntt: uniform residues (L, N).
+    """m, e: integer coefficient vectors (N,) or batches (B, N); s: secret (N,);
+    a_ntt: uniform residues (L, N) or (B, L, N).
 
-    Returns the ciphertext (2, L, N) in NTT form.
+    Returns the ciphertext(s) (2, L, N) or (B, 2, L, N) in NTT form.
     """
-    L = len(qs)
-    n = 1 << log_n
-    ct = np.empty((2, L, n), dtype=np.uint64)
-    me = [int(x) + int(y) for x, y in zip(m, e)]
+    m = np.asarray(m, dtype=object if isinstance(m, list) else None)
+    single = m.ndim == 1
+    m2 = m[None] if single else m
+    e2 = np.asarray(e)[None] if single else np.asarray(e)
+    a2 = np.asarray(a_ntt)[None] if single else np.asarray(a_ntt)
+    B, L, n = m2.shape[0], len(qs), 1 << log_n
+    ct = np.empty((B, 2, L, n), dtype=np.uint64)
     for l, (q, ps) in enumerate(zip(qs, psis)):
         qq = np.uint64(q)
         s_hat = ntt(_residues(s, q), q, ps, log_n)
-        me_hat = ntt(_residues(me, q), q, ps, log_n)
-        a = np.asarray(a_ntt[l], dtype=np.uint64) % qq
-        ct[1, l] = a
-        ct[0, l] = (me_hat + qq - (a * s_hat) % qq) % qq
-    return ct
+        me_hat = ntt((_residues(m2, q) + _residues(e2, q)) % qq, q, ps, log_n)     # (B, N)
+        a = a2[:, l].astype(np.uint64) % qq
+        ct[:, 1, l] = a
+        ct[:, 0, l] = (me_hat + qq - (a * s_hat) % qq) % qq
+    return ct[0] if single else ct
 
 
 def decrypt_residues(ct, s, qs, psis, log_n: int) -> np.ndarray:

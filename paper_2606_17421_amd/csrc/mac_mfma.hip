@@ -10,8 +10,9 @@
 // using (u + 0x80808080) ^ 0x80808080, whose bytes read as int8 are the digits.
 // Then  sum_i v_i x_i = sum_s 256^s S_s,  S_s = sum_{a+b=s} sum_i e_a(i) d_b(i),
 // where each S_s is an exact i32 contraction on v_mfma_i32_16x16x64_i8
-// (|S_s| <= 4 * d_in * 2^14 < 2^31 for d_in <= 16384).  The epilogue folds
-// sum_s S_s (256^s mod q) in i64 (< 7 * 2^60) and reduces once mod q.
+// (|S_s| <= 4 * d_in * 2^14 <= 2^30 for d_in <= 16384).  The epilogue folds
+// the classes in i64 (classes 0..3 with their exact weights 2^(8s), classes
+// 4..6 with 256^s mod q; |sum| < 2^62) and reduces once mod q.
 // Digit products: 12 per modular MAC with 3 weight digits, 16 with 4.
 //
 // Tiling: a 256-thread workgroup computes a 128 (rows) x 64 (columns) tile of
@@ -95,51 +96,77 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(
   if (threadIdx.x == 0) flags[l * mt_total + mt] = any ? 1u : 0u;
 }
 
+// K loop, software pipelined: while the MFMAs of step ks run, the raw
+// ciphertext residues and the weight fragments of step ks+1 are in flight;
+// the residues are then converted to digit fragments into the other LDS
+// buffer, so each step needs one barrier.
 template <int NDA>
 __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint32_t ks_total,
                                          const uint32_t* __restrict__ bsrc, size_t bstride,
-                                         uint32_t d_in, v4i (*bs)[4][64],
+                                         uint32_t d_in, v4i (*bs)[kNT][4][64],
                                          v4i (&acc)[kMT][kNT][7]) {
   const uint32_t tid = threadIdx.x;
   const uint32_t lane = tid & 63;
-  const uint32_t col = tid & 63;        // staging: column within the tile
-  const uint32_t g = tid >> 6;          // staging: 16-k group
-  for (uint32_t ks = 0; ks < ks_total; ++ks) {
-    // ---- stage B digits for this k-step ----
-    uint32_t p[16];
+  const uint32_t col = tid & 63;  // staging: column within the tile
+  const uint32_t g = tid >> 6;    // staging: 16-k group
+  uint32_t raw[16];
+  v4i a_cur[kMT][NDA], a_nxt[kMT][NDA];
+
+  auto load_b = [&](uint32_t ks) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       uint32_t k = ks * kBK + g * 16 + i;
-      k = k < d_in ? k : d_in - 1;      // padded k: any in-bounds value (its weight digits are 0)
-      p[i] = digits4(bsrc[static_cast<size_t>(k) * bstride + col]);
+      k = k < d_in ? k : d_in - 1;  // padded k: any in-bounds value (its weight digits are 0)
+      raw[i] = bsrc[static_cast<size_t>(k) * bstride + col];
     }
+  };
+  auto store_b = [&](int buf) {
+    uint32_t p[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) p[i] = digits4(raw[i]);
     v4i f[4];
     to_fragments(p, f);
-    __syncthreads();                    // previous step's readers are done
 #pragma unroll
-    for (int b = 0; b < 4; ++b) bs[col >> 4][b][(col & 15) + 16 * g] = f[b];
-    __syncthreads();
-    // ---- weight fragments (global, L2 resident) ----
-    v4i a[kMT][NDA];
+    for (int b = 0; b < 4; ++b) bs[buf][col >> 4][b][(col & 15) + 16 * g] = f[b];
+  };
+  auto load_a = [&](v4i (&a)[kMT][NDA], uint32_t ks) {
 #pragma unroll
     for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
       for (int d = 0; d < NDA; ++d)
         a[mt][d] = adig_wave[((static_cast<size_t>(mt) * ks_total + ks) * 4 + d) * 64 + lane];
-    // ---- contractions ----
+  };
+
+  load_b(0);
+  load_a(a_cur, 0);
+  store_b(0);
+  __syncthreads();
+  for (uint32_t ks = 0; ks < ks_total; ++ks) {
+    const int buf = ks & 1;
+    const bool more = ks + 1 < ks_total;
+    if (more) {
+      load_b(ks + 1);
+      load_a(a_nxt, ks + 1);
+    }
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt) {
       v4i bf[4];
 #pragma unroll
-      for (int b = 0; b < 4; ++b) bf[b] = bs[nt][b][lane];
+      for (int b = 0; b < 4; ++b) bf[b] = bs[buf][nt][b][lane];
 #pragma unroll
       for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
         for (int d = 0; d < NDA; ++d)
 #pragma unroll
           for (int b = 0; b < 4; ++b)
-            acc[mt][nt][d + b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[mt][d], bf[b], acc[mt][nt][d + b], 0, 0, 0);
+            acc[mt][nt][d + b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a_cur[mt][d], bf[b], acc[mt][nt][d + b], 0, 0, 0);
     }
+    if (more) store_b(buf ^ 1);
+    __syncthreads();
+#pragma unroll
+    for (int mt = 0; mt < kMT; ++mt)
+#pragma unroll
+      for (int d = 0; d < NDA; ++d) a_cur[mt][d] = a_nxt[mt][d];
   }
 }
 
@@ -147,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void mac_mfma_kernel(
     Tables tb, const v4i* __restrict__ adig, const uint32_t* __restrict__ flags,
     const uint32_t* __restrict__ ct_in, uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t d_in,
     uint32_t limbs, uint32_t mt_total, uint32_t ks_total, uint32_t tiles_m, uint32_t tiles_n) {
-  __shared__ v4i bs[kNT][4][64];  // B digit fragments of one k-step (16 KiB)
+  __shared__ v4i bs[2][kNT][4][64];  // B digit fragments, double buffered (32 KiB)
 
   // XCD-aware order: consecutive workgroup ids alternate XCDs; give each XCD a
   // contiguous range of logical tiles (row tile fastest, then column, then limb).
@@ -183,16 +210,15 @@ __global__ __launch_bounds__(kThreads) void mac_mfma_kernel(
   if (top) mac_loop<4>(adig_wave, ks_total, bsrc, bstride, d_in, bs, acc);
   else mac_loop<3>(adig_wave, ks_total, bsrc, bstride, d_in, bs, acc);
 
-  // ---- epilogue: out = sum_s S_s * (256^s mod q)  mod q ----
+  // ---- epilogue: out = sum_s S_s 256^s  mod q ----
+  // Classes 0..3 enter with their exact weights 2^(8s); classes 4..6 with
+  // 256^s mod q.  |v| < 2^62: the fp64 quotient estimate is within one of the
+  // true quotient, so the remainder, formed in 32 bits, lies in [-q, 2q).
   const uint32_t q = tb.q[l];
   const double qr = tb.q_recip[l];
-  int64_t cs[7];
-  uint64_t cpow = 1;
-#pragma unroll
-  for (int s = 0; s < 7; ++s) {
-    cs[s] = static_cast<int64_t>(cpow);
-    cpow = (cpow << 8) % q;
-  }
+  const int64_t c4 = static_cast<int64_t>((1ull << 32) % q);
+  const int64_t c5 = static_cast<int64_t>((static_cast<uint64_t>(c4) << 8) % q);
+  const int64_t c6 = static_cast<int64_t>((static_cast<uint64_t>(c5) << 8) % q);
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt) {
 #pragma unroll
@@ -202,13 +228,15 @@ __global__ __launch_bounds__(kThreads) void mac_mfma_kernel(
       uint32_t* orow = ct_out + ((static_cast<size_t>(j) * 2 + c) * limbs + l) * n + k0 + (lane & 15);
 #pragma unroll
       for (int nt = 0; nt < kNT; ++nt) {
-        int64_t v = 0;
-#pragma unroll
-        for (int s = 0; s < 7; ++s) v += static_cast<int64_t>(acc[mt][nt][s][r]) * cs[s];
-        const double qt = floor(static_cast<double>(v) * qr);
-        int64_t rem = v - static_cast<int64_t>(qt) * static_cast<int64_t>(q);
-        rem += rem < 0 ? static_cast<int64_t>(q) : 0;
-        rem -= rem >= static_cast<int64_t>(q) ? static_cast<int64_t>(q) : 0;
+        const v4i* a = acc[mt][nt];
+        int64_t v = static_cast<int64_t>(a[0][r]) + (static_cast<int64_t>(a[1][r]) << 8) +
+                    (static_cast<int64_t>(a[2][r]) << 16) + (static_cast<int64_t>(a[3][r]) << 24) +
+                    static_cast<int64_t>(a[4][r]) * c4 + static_cast<int64_t>(a[5][r]) * c5 +
+                    static_cast<int64_t>(a[6][r]) * c6;
+        const int64_t qt = static_cast<int64_t>(floor(static_cast<double>(v) * qr));
+        int32_t rem = static_cast<int32_t>(static_cast<uint32_t>(v) - static_cast<uint32_t>(qt) * q);
+        rem += rem < 0 ? static_cast<int32_t>(q) : 0;
+        rem -= rem >= static_cast<int32_t>(q) ? static_cast<int32_t>(q) : 0;
         orow[nt * 16] = static_cast<uint32_t>(rem);
       }
     }

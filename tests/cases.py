@@ -54,10 +54,8 @@ def build_layer(cfg: Config, *, log_n=None, limbs=None, d_in=None, d_out=None,
     s = gen.ternary_secret(st["secret"], n)
     a = gen.uniform_residues(st["residues"], (d_in,), qs, n)
     e = gen.gaussian_error(st["error"], (d_in, n))
-    ct = np.empty((d_in, 2, limbs, n), dtype=np.uint32)
-    for i in range(d_in):
-        m = encode.round_coeffs(encode.encode_coeffs(X[i], log_n), cfg.scale)
-        ct[i] = rlwe.encrypt(m, s, a[i], e[i], qs, psis, log_n).astype(np.uint32)
+    m_all = encode.round_coeffs(encode.encode_coeffs(X, log_n), cfg.scale)     # (d_in, N), one pass
+    ct = rlwe.encrypt(m_all, s, a, e, qs, psis, log_n).astype(np.uint32)       # (d_in, 2, L, N)
     return Layer(log_n, qs, psis, cfg.scale, W, X, s, ct)
 
 
@@ -91,9 +89,11 @@ def check_decrypted(layer: Layer, out_ct, rows, ref_slots, scale_out: float) -> 
     sd = rescale_noise_sd(layer.log_n, scale_out)
     sd_j = slot_noise_sd(layer, scale_out)
     worst, rms_re, rms_im = 0.0, [], []
+    ms = [rlwe.decrypt(np.asarray(out_ct[r], dtype=np.uint64), layer.s, layer.qs, layer.psis, layer.log_n)
+          for r in range(len(rows))]
+    zs = encode.decode(ms, scale_out, layer.log_n)                       # (rows, N/2), one pass
     for r, j in enumerate(rows):
-        m = rlwe.decrypt(np.asarray(out_ct[r], dtype=np.uint64), layer.s, layer.qs, layer.psis, layer.log_n)
-        z = encode.decode(m, scale_out, layer.log_n)
+        z = zs[r]
         err_re = z.real - ref_slots[r]
         worst = max(worst, np.max(np.abs(err_re) / sd_j), np.max(np.abs(z.imag) / sd_j))
         rms_re.append(np.mean(err_re ** 2))
