@@ -234,6 +234,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   std::vector<uint32_t> fwd(size_t(L) * n), fwds(size_t(L) * n), inv(size_t(L) * n), invs(size_t(L) * n);
   std::vector<uint32_t> ninv(L), ninvs(L), qinv(size_t(L) * L, 0), qinvs(size_t(L) * L, 0);
   std::vector<double> qrec(L);
+  std::vector<uint32_t> p256(size_t(L) * 8);
   for (uint32_t l = 0; l < L; ++l) {
     const uint64_t q = c->q[l];
     const uint64_t ps = c->psi[l];
@@ -254,6 +255,11 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
     ninv[l] = static_cast<uint32_t>(powmod(n, q - 2, q));
     ninvs[l] = shoup(ninv[l], c->q[l]);
     qrec[l] = 1.0 / static_cast<double>(q);
+    uint64_t pw = 1;
+    for (int e = 0; e < 8; ++e) {
+      p256[size_t(l) * 8 + e] = static_cast<uint32_t>(pw);
+      pw = (pw << 8) % q;
+    }
     for (uint32_t m = 0; m < L; ++m) {
       if (m == l) continue;
       const uint32_t v = static_cast<uint32_t>(powmod(c->q[m] % q, q - 2, q));
@@ -273,6 +279,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   const size_t o_qinv = blob.add(qinv.data(), qinv.size() * 4);
   const size_t o_qinvs = blob.add(qinvs.data(), qinvs.size() * 4);
   const size_t o_qrec = blob.add(qrec.data(), L * 8);
+  const size_t o_p256 = blob.add(p256.data(), p256.size() * 4);
   size_t o_perm = 0, o_fft = 0, o_rfft = 0, o_dct = 0;
   const bool enc = log_n <= 15;
   if (enc) {
@@ -335,6 +342,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   t.qinv = reinterpret_cast<const uint32_t*>(base + o_qinv);
   t.qinv_shoup = reinterpret_cast<const uint32_t*>(base + o_qinvs);
   t.q_recip = reinterpret_cast<const double*>(base + o_qrec);
+  t.pow256 = reinterpret_cast<const uint32_t*>(base + o_p256);
   if (enc) {
     t.slot_perm = reinterpret_cast<const uint32_t*>(base + o_perm);
     t.fft_tw = reinterpret_cast<const double2*>(base + o_fft);
@@ -470,10 +478,10 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc, const uin
   }
   const bool mfma_ok = ckks::mac_mfma_supported(d_in);
   if (ctx->mac_algo == CKKS_MAC_MFMA && !mfma_ok)
-    return fail(CKKS_E_UNSUPPORTED, "matrix-core MAC needs d_in <= 16384 (got %u)", d_in);
+    return fail(CKKS_E_UNSUPPORTED, "matrix-core MAC needs d_in <= 4096 (got %u)", d_in);
   const bool use_mfma = ctx->mac_algo == CKKS_MAC_MFMA || (ctx->mac_algo == CKKS_MAC_AUTO && mfma_ok);
   if (use_mfma) {
-    const size_t need = ckks::mac_mfma_workspace_bytes(d_out, d_in, limbs);
+    const size_t need = ckks::mac_mfma_workspace_bytes(ctx->n, d_out, d_in, limbs);
     if (!workspace || workspace_bytes < need)
       return fail(CKKS_E_WORKSPACE, "MAC workspace %zu bytes < %zu required", workspace_bytes, need);
     if (!aligned16(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 16-byte aligned");
@@ -526,7 +534,7 @@ size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b,
   if (!ctx || limbs < 1 || limbs > ctx->L) return static_cast<size_t>(-1);
   switch (op) {
     case CKKS_OP_MAC_SCALAR:
-      return ctx->mac_algo == CKKS_MAC_VALU ? 0 : ckks::mac_mfma_workspace_bytes(a, b, limbs);
+      return ctx->mac_algo == CKKS_MAC_VALU ? 0 : ckks::mac_mfma_workspace_bytes(ctx->n, a, b, limbs);
     case CKKS_OP_RESCALE:
       return limbs < 2 ? static_cast<size_t>(-1) : ckks::rescale_workspace_bytes(ctx->t, a);
     case CKKS_OP_ENCODE_POLY:

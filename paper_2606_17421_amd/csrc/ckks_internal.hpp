@@ -29,6 +29,7 @@ struct Tables {
   const uint32_t* qinv;        // [L][L]  qinv[m*L + l] = q_m^-1 mod q_l (0 on the diagonal)
   const uint32_t* qinv_shoup;  // [L][L]
   const double* q_recip;       // [L]     1.0 / q_l rounded to nearest
+  const uint32_t* pow256;      // [L][8]  256^s mod q_l, s < 8
   // Encode tables (present when log_n <= 15; M = N/2, P = N/4).
   const uint32_t* slot_perm;   // [M]  slot index j whose odd exponent is 2u+1 (up to sign)
   const double2* fft_tw;       // [P/2] exp(-2 pi i m / P)
@@ -102,7 +103,7 @@ hipError_t launch_mac_scalar_valu(const Tables& t, const uint32_t* w_enc, const 
                                   uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
                                   hipStream_t s);
 
-size_t mac_mfma_workspace_bytes(uint32_t d_out, uint32_t d_in, uint32_t limbs);
+size_t mac_mfma_workspace_bytes(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs);
 bool mac_mfma_supported(uint32_t d_in);
 hipError_t launch_mac_scalar_mfma(const Tables& t, const uint32_t* w_enc, const uint32_t* ct_in,
                                   uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,

@@ -10,20 +10,28 @@
 // using (u + 0x80808080) ^ 0x80808080, whose bytes read as int8 are the digits.
 // Then  sum_i v_i x_i = sum_s 256^s S_s,  S_s = sum_{a+b=s} sum_i e_a(i) d_b(i),
 // where each S_s is an exact i32 contraction on v_mfma_i32_16x16x64_i8
-// (|S_s| <= 4 * d_in * 2^14 <= 2^30 for d_in <= 16384).  The epilogue folds
-// the classes in i64 (classes 0..3 with their exact weights 2^(8s), classes
-// 4..6 with 256^s mod q; |sum| < 2^62) and reduces once mod q.
+// (|S_s| <= 4 * d_in * 2^14 <= 2^28 for d_in <= 4096).  The epilogue folds the
+// classes with exact fp64 integer arithmetic: classes 0..3 with their weights
+// 2^(8s) (a sum below 2^52.01), classes 4..6 with 256^s mod q split into 15-bit
+// halves, one intermediate reduction, then one final reduction mod q.
 // Digit products: 12 per modular MAC with 3 weight digits, 16 with 4.
 //
-// Tiling: a 256-thread workgroup computes a 128 (rows) x 64 (columns) tile of
-// one limb; each wave owns 32 rows x 64 columns (2 x 4 MFMA tiles x 6 or 7
-// shift-class accumulators).  Weight digit fragments are pre-arranged in
-// MFMA lane order by a prep kernel and read straight from global memory (L2
-// resident); ciphertext residues are staged through LDS, converted to digit
-// fragments once per workgroup.  Workgroups are ordered (limb, column tile,
-// row tile) with row tiles fastest and remapped so that each XCD runs a
-// contiguous range: tiles sharing a B tile, and a whole limb's A, stay in one
-// XCD's L2.
+// Two prep kernels lay both operands out as MFMA fragments (16 bytes per lane,
+// the lane order of v_mfma_i32_16x16x64_i8): the weights per 16-row tile (with
+// a flag for tiles that need a fourth digit), the ciphertext residues per
+// 64-column tile and 64-deep k-step.  The residue conversion is a streaming
+// pass (read 4 B, write 4 B per residue) done once, instead of once per row
+// tile inside the contraction.
+//
+// Contraction: a 256-thread workgroup computes a 128 (rows) x 64 (columns)
+// tile of one limb; each wave owns 32 rows x 64 columns (2 x 4 MFMA tiles x 6
+// or 7 shift-class accumulators in AGPRs).  Per 64-deep k-step the workgroup
+// copies the 16 KiB of ciphertext digit fragments into an LDS double buffer
+// (loads issued two steps ahead) and each wave reads its weight fragments
+// from global memory (L2 resident; issued one step ahead).  Workgroups are
+// ordered (limb, column tile, row tile) with row tiles fastest and remapped so
+// that each XCD runs a contiguous range: tiles sharing a column tile, and a
+// whole limb's weights, stay in one XCD's L2.
 #include "ckks_internal.hpp"
 
 namespace ckks {
@@ -33,32 +41,41 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kBM = 128;       // rows per workgroup tile
-constexpr int kBN = 64;        // columns per workgroup tile
+constexpr int kBN = 32;        // columns per workgroup tile
 constexpr int kBK = 64;        // K per MFMA step
 constexpr int kMT = 2;         // 16-row MFMA tiles per wave
 constexpr int kNT = kBN / 16;  // 16-column MFMA tiles per wave
+constexpr int kFragsPerStep = kNT * 4 * 64;  // 16-byte ciphertext fragments per k-step
+constexpr int kBprepThreads = kBN * 4;       // one thread per (column, 16-k group)
 constexpr uint32_t kBias = 0x80808080u;
-constexpr uint32_t kMaxDin = 16384;
+constexpr uint32_t kMaxDin = 4096;
 
-__device__ __forceinline__ uint32_t digits4(uint32_t u) { return (u + kBias) ^ kBias; }
 
-// o[b] byte e = p[e] byte b  (4x4 byte transpose)
-__device__ __forceinline__ void transpose4(const uint32_t (&p)[4], uint32_t (&o)[4]) {
-#pragma unroll
-  for (int b = 0; b < 4; ++b)
-    o[b] = ((p[0] >> (8 * b)) & 0xffu) | (((p[1] >> (8 * b)) & 0xffu) << 8) |
-           (((p[2] >> (8 * b)) & 0xffu) << 16) | (((p[3] >> (8 * b)) & 0xffu) << 24);
+// o[b] byte e = p[e] byte b (4x4 byte transpose, eight v_perm_b32).
+// __builtin_amdgcn_perm(hi, lo, sel): selector byte values 0-3 pick bytes of
+// lo, 4-7 bytes of hi.
+__device__ __forceinline__ void transpose4(uint32_t p0, uint32_t p1, uint32_t p2, uint32_t p3,
+                                           uint32_t (&o)[4]) {
+  const uint32_t x01l = __builtin_amdgcn_perm(p1, p0, 0x05010400u);  // p0.0 p1.0 p0.1 p1.1
+  const uint32_t x01h = __builtin_amdgcn_perm(p1, p0, 0x07030602u);  // p0.2 p1.2 p0.3 p1.3
+  const uint32_t x23l = __builtin_amdgcn_perm(p3, p2, 0x05010400u);
+  const uint32_t x23h = __builtin_amdgcn_perm(p3, p2, 0x07030602u);
+  o[0] = __builtin_amdgcn_perm(x23l, x01l, 0x05040100u);            // p0.0 p1.0 p2.0 p3.0
+  o[1] = __builtin_amdgcn_perm(x23l, x01l, 0x07060302u);            // p0.1 p1.1 p2.1 p3.1
+  o[2] = __builtin_amdgcn_perm(x23h, x01h, 0x05040100u);
+  o[3] = __builtin_amdgcn_perm(x23h, x01h, 0x07060302u);
 }
 
-// 16 packed digit words (consecutive k) -> one 16-byte fragment per digit.
-__device__ __forceinline__ void to_fragments(const uint32_t (&p)[16], v4i (&f)[4]) {
+// 16 residues (consecutive k) -> one 16-byte digit fragment per digit b:
+// byte i of fragment b is digit b of residue i.  The bias is added before
+// the byte transpose and removed after it (both are bytewise).
+__device__ __forceinline__ void to_fragments(const uint32_t (&x)[16], v4i (&f)[4]) {
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    const uint32_t in[4] = {p[4 * g], p[4 * g + 1], p[4 * g + 2], p[4 * g + 3]};
     uint32_t o[4];
-    transpose4(in, o);
+    transpose4(x[4 * g] + kBias, x[4 * g + 1] + kBias, x[4 * g + 2] + kBias, x[4 * g + 3] + kBias, o);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) f[b][g] = static_cast<int>(o[b]);
+    for (int b = 0; b < 4; ++b) f[b][g] = static_cast<int>(o[b] ^ kBias);
   }
 }
 
@@ -82,8 +99,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(
       const uint32_t k = k0 + i;
       uint32_t w = 0;
       if (row < d_out && k < d_in) w = w_enc[(static_cast<size_t>(row) * d_in + k) * limbs + l];
-      const uint32_t v = w > (q >> 1) ? w - q : w;  // centred, two's complement
-      p[i] = digits4(v);
+      p[i] = w > (q >> 1) ? w - q : w;  // centred, two's complement
     }
     v4i f[4];
     to_fragments(p, f);
@@ -96,85 +112,161 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(
   if (threadIdx.x == 0) flags[l * mt_total + mt] = any ? 1u : 0u;
 }
 
-// K loop, software pipelined: while the MFMAs of step ks run, the raw
-// ciphertext residues and the weight fragments of step ks+1 are in flight;
-// the residues are then converted to digit fragments into the other LDS
-// buffer, so each step needs one barrier.
+// Ciphertext digits: bdig[((l * tiles_n + t) * ks_total + ks) * kFragsPerStep + f]
+// (16-byte units), f = (nt * 4 + b) * 64 + lane for the 16-column tile nt of
+// column tile t, digit b, and MFMA lane = col%16 + 16 * (k%64 / 16);
+// byte i holds digit b of residue k = ks*64 + 16*(lane/16) + i (0 past d_in).
+__global__ __launch_bounds__(kBprepThreads) void mfma_bprep_kernel(
+    const uint32_t* __restrict__ ct_in, uint32_t d_in, uint32_t limbs, uint32_t log_n,
+    uint32_t tiles_n, uint32_t ks_total, v4i* __restrict__ bdig) {
+  const uint32_t ks = blockIdx.x % ks_total;
+  const uint32_t t64 = (blockIdx.x / ks_total) % tiles_n;
+  const uint32_t l = blockIdx.x / (ks_total * tiles_n);
+  const uint32_t n = 1u << log_n;
+  const uint32_t col = threadIdx.x % kBN, g = threadIdx.x / kBN;
+  const uint32_t gcol = t64 * kBN + col;                     // column in [0, 2N)
+  const uint32_t c = gcol >> log_n, kk = gcol & (n - 1);
+  const size_t stride = 2ull * limbs * n;                    // one input ciphertext
+  const uint32_t* src = ct_in + (static_cast<size_t>(c) * limbs + l) * n + kk;
+  uint32_t x[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const uint32_t k = ks * kBK + g * 16 + i;
+    x[i] = k < d_in ? src[static_cast<size_t>(k) * stride] : 0u;
+  }
+  v4i f[4];
+  to_fragments(x, f);
+  v4i* dst = bdig + ((static_cast<size_t>(l) * tiles_n + t64) * ks_total + ks) * kFragsPerStep;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) dst[((col >> 4) * 4 + b) * 64 + (col & 15) + 16 * g] = f[b];
+}
+
+// K loop.  Step ks: issue the fragment copies of step ks+2 (register set
+// ks%2) and the weight fragments of step ks+1; contract step ks out of LDS
+// buffer ks%2; then store the copies of step ks+1 (issued two steps earlier)
+// into LDS buffer (ks+1)%2 and synchronise once.
 template <int NDA>
 __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint32_t ks_total,
-                                         const uint32_t* __restrict__ bsrc, size_t bstride,
-                                         uint32_t d_in, v4i (*bs)[kNT][4][64],
-                                         v4i (&acc)[kMT][kNT][7]) {
+                                         const v4i* __restrict__ bsrc, v4i (*bs)[kFragsPerStep],
+                                         v4i (&acc)[kMT][kNT][NDA + 3]) {
   const uint32_t tid = threadIdx.x;
   const uint32_t lane = tid & 63;
-  const uint32_t col = tid & 63;  // staging: column within the tile
-  const uint32_t g = tid >> 6;    // staging: 16-k group
-  uint32_t raw[16];
+  constexpr int kCopy = kFragsPerStep / kThreads;  // 16-byte copies per thread per k-step
+  v4i rb[2][kCopy];
   v4i a_cur[kMT][NDA], a_nxt[kMT][NDA];
 
-  auto load_b = [&](uint32_t ks) {
+  auto load_b = [&](v4i (&r)[kCopy], uint32_t ks) {
+    const v4i* p = bsrc + static_cast<size_t>(ks) * kFragsPerStep;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      uint32_t k = ks * kBK + g * 16 + i;
-      k = k < d_in ? k : d_in - 1;  // padded k: any in-bounds value (its weight digits are 0)
-      raw[i] = bsrc[static_cast<size_t>(k) * bstride + col];
-    }
+    for (int j = 0; j < kCopy; ++j) r[j] = p[tid + kThreads * j];
   };
-  auto store_b = [&](int buf) {
-    uint32_t p[16];
+  auto store_b = [&](const v4i (&r)[kCopy], int buf) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) p[i] = digits4(raw[i]);
-    v4i f[4];
-    to_fragments(p, f);
-#pragma unroll
-    for (int b = 0; b < 4; ++b) bs[buf][col >> 4][b][(col & 15) + 16 * g] = f[b];
+    for (int j = 0; j < kCopy; ++j) bs[buf][tid + kThreads * j] = r[j];
   };
   auto load_a = [&](v4i (&a)[kMT][NDA], uint32_t ks) {
 #pragma unroll
     for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
       for (int d = 0; d < NDA; ++d)
-        a[mt][d] = adig_wave[((static_cast<size_t>(mt) * ks_total + ks) * 4 + d) * 64 + lane];
+        a[mt][d] = (adig_wave + ((static_cast<size_t>(mt) * ks_total + ks) * 4 + d) * 64)[lane];
   };
-
-  load_b(0);
-  load_a(a_cur, 0);
-  store_b(0);
-  __syncthreads();
-  for (uint32_t ks = 0; ks < ks_total; ++ks) {
+  auto step = [&](uint32_t ks, v4i (&rb_issue)[kCopy], v4i (&rb_store)[kCopy]) {
     const int buf = ks & 1;
-    const bool more = ks + 1 < ks_total;
-    if (more) {
-      load_b(ks + 1);
-      load_a(a_nxt, ks + 1);
+    if (ks + 2 < ks_total) load_b(rb_issue, ks + 2);
+    if (ks + 1 < ks_total) load_a(a_nxt, ks + 1);
+    __builtin_amdgcn_sched_barrier(0);  // keep the prefetches ahead of the contractions
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      v4i bf[kNT];
+#pragma unroll
+      for (int nt = 0; nt < kNT; ++nt) bf[nt] = bs[buf][(nt * 4 + b) * 64 + lane];
+      // within one digit b the NDA * kMT * kNT contractions hit distinct accumulators
+#pragma unroll
+      for (int d = 0; d < NDA; ++d)
+#pragma unroll
+        for (int mt = 0; mt < kMT; ++mt)
+#pragma unroll
+          for (int nt = 0; nt < kNT; ++nt)
+            acc[mt][nt][d + b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a_cur[mt][d], bf[nt], acc[mt][nt][d + b], 0, 0, 0);
     }
-#pragma unroll
-    for (int nt = 0; nt < kNT; ++nt) {
-      v4i bf[4];
-#pragma unroll
-      for (int b = 0; b < 4; ++b) bf[b] = bs[buf][nt][b][lane];
-#pragma unroll
-      for (int mt = 0; mt < kMT; ++mt)
-#pragma unroll
-        for (int d = 0; d < NDA; ++d)
-#pragma unroll
-          for (int b = 0; b < 4; ++b)
-            acc[mt][nt][d + b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a_cur[mt][d], bf[b], acc[mt][nt][d + b], 0, 0, 0);
-    }
-    if (more) store_b(buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (ks + 1 < ks_total) store_b(rb_store, buf ^ 1);
     __syncthreads();
 #pragma unroll
     for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
       for (int d = 0; d < NDA; ++d) a_cur[mt][d] = a_nxt[mt][d];
+  };
+
+  load_b(rb[0], 0);
+  if (ks_total > 1) load_b(rb[1], 1);
+  load_a(a_cur, 0);
+  store_b(rb[0], 0);
+  __syncthreads();
+  uint32_t ks = 0;
+  for (; ks + 1 < ks_total; ks += 2) {
+    step(ks, rb[0], rb[1]);      // issues ks+2 into set 0, stores ks+1 from set 1
+    step(ks + 1, rb[1], rb[0]);  // issues ks+3 into set 1, stores ks+2 from set 0
+  }
+  if (ks < ks_total) step(ks, rb[0], rb[1]);
+}
+
+// out = sum_s S_s 256^s mod q, exactly, in fp64 integer arithmetic.
+template <int NDA>
+__device__ __forceinline__ void epilogue(const v4i (&acc)[kMT][kNT][NDA + 3], const Tables& tb, uint32_t l,
+                                         uint32_t mt_wave, uint32_t lane, uint32_t d_out, uint32_t c,
+                                         uint32_t limbs, uint32_t k0, uint32_t* __restrict__ ct_out) {
+  const uint32_t n = tb.n;
+  const uint32_t qi = tb.q[l];
+  const double q = static_cast<double>(qi);
+  const double qr = tb.q_recip[l];
+  const uint32_t* pw = tb.pow256 + l * 8;
+  const double c4h = static_cast<double>(pw[4] >> 15), c4l = static_cast<double>(pw[4] & 0x7fffu);
+  const double c5h = static_cast<double>(pw[5] >> 15), c5l = static_cast<double>(pw[5] & 0x7fffu);
+  const double c6h = static_cast<double>(pw[6] >> 15), c6l = static_cast<double>(pw[6] & 0x7fffu);
+#pragma unroll
+  for (int mt = 0; mt < kMT; ++mt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint32_t j = (mt_wave + mt) * 16 + 4 * (lane >> 4) + r;
+      if (j >= d_out) continue;
+      uint32_t* orow = ct_out + ((static_cast<size_t>(j) * 2 + c) * limbs + l) * n + k0 + (lane & 15);
+#pragma unroll
+      for (int nt = 0; nt < kNT; ++nt) {
+        const v4i* a = acc[mt][nt];
+        // classes 0..3: exact (|sum| < 2^52.01)
+        const double vlo = fma(static_cast<double>(a[3][r]), 16777216.0,
+                               fma(static_cast<double>(a[2][r]), 65536.0,
+                                   fma(static_cast<double>(a[1][r]), 256.0, static_cast<double>(a[0][r]))));
+        // classes 4..6 with 256^s mod q = ch 2^15 + cl (each partial sum < 2^45, exact)
+        const double a4 = static_cast<double>(a[4][r]), a5 = static_cast<double>(a[5][r]);
+        double th = fma(a5, c5h, a4 * c4h);
+        double tl = fma(a5, c5l, a4 * c4l);
+        if constexpr (NDA == 4) {
+          const double a6 = static_cast<double>(a[6][r]);
+          th = fma(a6, c6h, th);
+          tl = fma(a6, c6l, tl);
+        }
+        const double rh = fma(-floor(th * qr), q, th);         // th mod q, in (-q, 2q)
+        const double v = fma(rh, 32768.0, vlo + tl);            // |v| < 2^52.2, exact
+        double rem = fma(-floor(v * qr), q, v);                 // in [-q, 2q)
+        rem += rem < 0.0 ? q : 0.0;
+        rem -= rem >= q ? q : 0.0;
+        orow[nt * 16] = static_cast<uint32_t>(rem);
+      }
+    }
   }
 }
 
-__global__ __launch_bounds__(kThreads) void mac_mfma_kernel(
+// One instantiation per weight-digit count; both are launched over the full
+// grid and a workgroup exits at once unless its row tile's flag selects it.
+template <int NDA>
+__global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
     Tables tb, const v4i* __restrict__ adig, const uint32_t* __restrict__ flags,
-    const uint32_t* __restrict__ ct_in, uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t d_in,
-    uint32_t limbs, uint32_t mt_total, uint32_t ks_total, uint32_t tiles_m, uint32_t tiles_n) {
-  __shared__ v4i bs[2][kNT][4][64];  // B digit fragments, double buffered (32 KiB)
+    const v4i* __restrict__ bdig, uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t limbs,
+    uint32_t mt_total, uint32_t ks_total, uint32_t tiles_m, uint32_t tiles_n) {
+  __shared__ v4i bs[2][kFragsPerStep];  // ciphertext digit fragments of one k-step, double buffered
 
   // XCD-aware order: consecutive workgroup ids alternate XCDs; give each XCD a
   // contiguous range of logical tiles (row tile fastest, then column, then limb).
@@ -186,84 +278,54 @@ __global__ __launch_bounds__(kThreads) void mac_mfma_kernel(
   const uint32_t ntile = lid % tiles_n;
   const uint32_t l = lid / tiles_n;
 
-  const uint32_t n = tb.n;
-  const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const uint32_t col0 = ntile * kBN;  // column in [0, 2N): component c = col0 / N
-  const uint32_t c = col0 >> tb.log_n, k0 = col0 & (n - 1);
-  const size_t bstride = 2ull * limbs * n;  // one input ciphertext
-  const uint32_t* bsrc = ct_in + (static_cast<size_t>(c) * limbs + l) * n + k0;
-  const uint32_t mt_wave = mtile * (kBM / 16) + wave * kMT;
-  const v4i* adig_wave = adig + (static_cast<size_t>(l) * mt_total + mt_wave) * ks_total * 4 * 64;
-
   uint32_t top = 0;
 #pragma unroll
   for (int i = 0; i < kBM / 16; ++i) top |= flags[l * mt_total + mtile * (kBM / 16) + i];
+  if ((top != 0) != (NDA == 4)) return;  // workgroup-uniform
 
-  v4i acc[kMT][kNT][7];
+  const uint32_t n = tb.n;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const uint32_t col0 = ntile * kBN;  // column in [0, 2N): component c = col0 / N
+  const uint32_t c = col0 >> tb.log_n, k0 = col0 & (n - 1);
+  const v4i* bsrc = bdig + (static_cast<size_t>(l) * tiles_n + ntile) * ks_total * kFragsPerStep;
+  const uint32_t mt_wave = mtile * (kBM / 16) + wave * kMT;
+  const v4i* adig_wave = adig + (static_cast<size_t>(l) * mt_total + mt_wave) * ks_total * 4 * 64;
+
+  v4i acc[kMT][kNT][NDA + 3];
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
-      for (int s = 0; s < 7; ++s) acc[mt][nt][s] = v4i{0, 0, 0, 0};
+      for (int s = 0; s < NDA + 3; ++s) acc[mt][nt][s] = v4i{0, 0, 0, 0};
 
-  if (top) mac_loop<4>(adig_wave, ks_total, bsrc, bstride, d_in, bs, acc);
-  else mac_loop<3>(adig_wave, ks_total, bsrc, bstride, d_in, bs, acc);
-
-  // ---- epilogue: out = sum_s S_s 256^s  mod q ----
-  // Classes 0..3 enter with their exact weights 2^(8s); classes 4..6 with
-  // 256^s mod q.  |v| < 2^62: the fp64 quotient estimate is within one of the
-  // true quotient, so the remainder, formed in 32 bits, lies in [-q, 2q).
-  const uint32_t q = tb.q[l];
-  const double qr = tb.q_recip[l];
-  const int64_t c4 = static_cast<int64_t>((1ull << 32) % q);
-  const int64_t c5 = static_cast<int64_t>((static_cast<uint64_t>(c4) << 8) % q);
-  const int64_t c6 = static_cast<int64_t>((static_cast<uint64_t>(c5) << 8) % q);
-#pragma unroll
-  for (int mt = 0; mt < kMT; ++mt) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const uint32_t j = (mt_wave + mt) * 16 + 4 * (lane >> 4) + r;
-      if (j >= d_out) continue;
-      uint32_t* orow = ct_out + ((static_cast<size_t>(j) * 2 + c) * limbs + l) * n + k0 + (lane & 15);
-#pragma unroll
-      for (int nt = 0; nt < kNT; ++nt) {
-        const v4i* a = acc[mt][nt];
-        int64_t v = static_cast<int64_t>(a[0][r]) + (static_cast<int64_t>(a[1][r]) << 8) +
-                    (static_cast<int64_t>(a[2][r]) << 16) + (static_cast<int64_t>(a[3][r]) << 24) +
-                    static_cast<int64_t>(a[4][r]) * c4 + static_cast<int64_t>(a[5][r]) * c5 +
-                    static_cast<int64_t>(a[6][r]) * c6;
-        const int64_t qt = static_cast<int64_t>(floor(static_cast<double>(v) * qr));
-        int32_t rem = static_cast<int32_t>(static_cast<uint32_t>(v) - static_cast<uint32_t>(qt) * q);
-        rem += rem < 0 ? static_cast<int32_t>(q) : 0;
-        rem -= rem >= static_cast<int32_t>(q) ? static_cast<int32_t>(q) : 0;
-        orow[nt * 16] = static_cast<uint32_t>(rem);
-      }
-    }
-  }
+  mac_loop<NDA>(adig_wave, ks_total, bsrc, bs, acc);
+  epilogue<NDA>(acc, tb, l, mt_wave, lane, d_out, c, limbs, k0, ct_out);
 }
 
 struct Shape {
-  uint32_t tiles_m, mt_total, ks_total;
-  size_t adig_bytes, flag_bytes;
+  uint32_t tiles_m, tiles_n, mt_total, ks_total;
+  size_t adig_bytes, flag_bytes, bdig_bytes;
 };
 
-Shape shape_of(uint32_t d_out, uint32_t d_in, uint32_t limbs) {
+Shape shape_of(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
   Shape s;
   s.tiles_m = (d_out + kBM - 1) / kBM;
+  s.tiles_n = 2 * n / kBN;
   s.mt_total = s.tiles_m * (kBM / 16);
   s.ks_total = (d_in + kBK - 1) / kBK;
   s.adig_bytes = static_cast<size_t>(limbs) * s.mt_total * s.ks_total * 4 * 64 * sizeof(v4i);
   s.flag_bytes = ((static_cast<size_t>(limbs) * s.mt_total * 4) + 255) & ~size_t(255);
+  s.bdig_bytes = static_cast<size_t>(limbs) * s.tiles_n * s.ks_total * kFragsPerStep * sizeof(v4i);
   return s;
 }
 
 }  // namespace
 
-size_t mac_mfma_workspace_bytes(uint32_t d_out, uint32_t d_in, uint32_t limbs) {
+size_t mac_mfma_workspace_bytes(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
   if (d_out == 0 || d_in == 0 || d_in > kMaxDin) return 0;
-  const Shape s = shape_of(d_out, d_in, limbs);
-  return s.adig_bytes + s.flag_bytes;
+  const Shape s = shape_of(n, d_out, d_in, limbs);
+  return s.adig_bytes + s.flag_bytes + s.bdig_bytes;
 }
 
 bool mac_mfma_supported(uint32_t d_in) { return d_in >= 1 && d_in <= kMaxDin; }
@@ -271,16 +333,21 @@ bool mac_mfma_supported(uint32_t d_in) { return d_in >= 1 && d_in <= kMaxDin; }
 hipError_t launch_mac_scalar_mfma(const Tables& t, const uint32_t* w_enc, const uint32_t* ct_in,
                                   uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
                                   void* workspace, hipStream_t st) {
-  const Shape s = shape_of(d_out, d_in, limbs);
-  v4i* adig = static_cast<v4i*>(workspace);
-  uint32_t* flags = reinterpret_cast<uint32_t*>(static_cast<unsigned char*>(workspace) + s.adig_bytes);
+  const Shape s = shape_of(t.n, d_out, d_in, limbs);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  v4i* adig = reinterpret_cast<v4i*>(ws);
+  uint32_t* flags = reinterpret_cast<uint32_t*>(ws + s.adig_bytes);
+  v4i* bdig = reinterpret_cast<v4i*>(ws + s.adig_bytes + s.flag_bytes);
   mfma_prep_kernel<<<dim3(s.mt_total, limbs), kThreads, 0, st>>>(t.q, w_enc, d_out, d_in, limbs, s.mt_total,
                                                                  s.ks_total, adig, flags);
-  const uint32_t tiles_n = 2 * t.n / kBN;
-  const size_t grid = static_cast<size_t>(limbs) * tiles_n * s.tiles_m;
-  mac_mfma_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, ct_in, ct_out, d_out, d_in,
-                                                                   limbs, s.mt_total, s.ks_total, s.tiles_m,
-                                                                   tiles_n);
+  const size_t bgrid = static_cast<size_t>(limbs) * s.tiles_n * s.ks_total;
+  mfma_bprep_kernel<<<static_cast<uint32_t>(bgrid), kBprepThreads, 0, st>>>(ct_in, d_in, limbs, t.log_n, s.tiles_n,
+                                                                      s.ks_total, bdig);
+  const size_t grid = static_cast<size_t>(limbs) * s.tiles_n * s.tiles_m;
+  mac_mfma_kernel<3><<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, bdig, ct_out, d_out, limbs,
+                                                                      s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
+  mac_mfma_kernel<4><<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, bdig, ct_out, d_out, limbs,
+                                                                      s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
   return hipGetLastError();
 }
 
