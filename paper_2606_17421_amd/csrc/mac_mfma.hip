@@ -46,7 +46,7 @@ constexpr int kBK = 64;        // K per MFMA step
 constexpr int kMT = 2;         // 16-row MFMA tiles per wave
 constexpr int kNT = kBN / 16;  // 16-column MFMA tiles per wave
 constexpr int kFragsPerStep = kNT * 4 * 64;  // 16-byte ciphertext fragments per k-step
-constexpr int kBprepThreads = kBN * 4;       // one thread per (column, 16-k group)
+constexpr int kGroupM = 8;                   // row tiles per L2-resident weight group
 constexpr uint32_t kBias = 0x80808080u;
 constexpr uint32_t kMaxDin = 4096;
 
@@ -112,57 +112,48 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(
   if (threadIdx.x == 0) flags[l * mt_total + mt] = any ? 1u : 0u;
 }
 
-// Ciphertext digits: bdig[((l * tiles_n + t) * ks_total + ks) * kFragsPerStep + f]
-// (16-byte units), f = (nt * 4 + b) * 64 + lane for the 16-column tile nt of
-// column tile t, digit b, and MFMA lane = col%16 + 16 * (k%64 / 16);
-// byte i holds digit b of residue k = ks*64 + 16*(lane/16) + i (0 past d_in).
-__global__ __launch_bounds__(kBprepThreads) void mfma_bprep_kernel(
-    const uint32_t* __restrict__ ct_in, uint32_t d_in, uint32_t limbs, uint32_t log_n,
-    uint32_t tiles_n, uint32_t ks_total, v4i* __restrict__ bdig) {
-  const uint32_t ks = blockIdx.x % ks_total;
-  const uint32_t t64 = (blockIdx.x / ks_total) % tiles_n;
-  const uint32_t l = blockIdx.x / (ks_total * tiles_n);
-  const uint32_t n = 1u << log_n;
-  const uint32_t col = threadIdx.x % kBN, g = threadIdx.x / kBN;
-  const uint32_t gcol = t64 * kBN + col;                     // column in [0, 2N)
-  const uint32_t c = gcol >> log_n, kk = gcol & (n - 1);
-  const size_t stride = 2ull * limbs * n;                    // one input ciphertext
-  const uint32_t* src = ct_in + (static_cast<size_t>(c) * limbs + l) * n + kk;
-  uint32_t x[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const uint32_t k = ks * kBK + g * 16 + i;
-    x[i] = k < d_in ? src[static_cast<size_t>(k) * stride] : 0u;
-  }
-  v4i f[4];
-  to_fragments(x, f);
-  v4i* dst = bdig + ((static_cast<size_t>(l) * tiles_n + t64) * ks_total + ks) * kFragsPerStep;
-#pragma unroll
-  for (int b = 0; b < 4; ++b) dst[((col >> 4) * 4 + b) * 64 + (col & 15) + 16 * g] = f[b];
-}
-
-// K loop.  Step ks: issue the fragment copies of step ks+2 (register set
-// ks%2) and the weight fragments of step ks+1; contract step ks out of LDS
-// buffer ks%2; then store the copies of step ks+1 (issued two steps earlier)
-// into LDS buffer (ks+1)%2 and synchronise once.
+// K loop.  The workgroup converts each 64-deep k-step of its 32 ciphertext
+// columns into digit fragments in LDS (thread: one column, 8 consecutive k);
+// the other workgroup resident on the CU runs its contractions meanwhile.
+// Step ks: issue the residue loads of step ks+2 (register set ks%2) and the
+// weight fragments of step ks+1; contract step ks out of LDS buffer ks%2;
+// convert the residues of step ks+1 (issued two steps earlier) into LDS
+// buffer (ks+1)%2; synchronise once.
 template <int NDA>
 __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint32_t ks_total,
-                                         const v4i* __restrict__ bsrc, v4i (*bs)[kFragsPerStep],
+                                         const uint32_t* __restrict__ bsrc, size_t bstride,
+                                         uint32_t d_in, v4i (*bs)[kFragsPerStep],
                                          v4i (&acc)[kMT][kNT][NDA + 3]) {
   const uint32_t tid = threadIdx.x;
   const uint32_t lane = tid & 63;
-  constexpr int kCopy = kFragsPerStep / kThreads;  // 16-byte copies per thread per k-step
-  v4i rb[2][kCopy];
+  const uint32_t col = tid % kBN;       // staging: column of the tile
+  const uint32_t kg = tid / kBN;        // staging: 8-k group within the step (0..7)
+  uint32_t raw[2][8];
   v4i a_cur[kMT][NDA], a_nxt[kMT][NDA];
+  // LDS byte offset of this thread's 8 bytes of digit-b fragment: fragment
+  // (nt, b), MFMA lane col%16 + 16*(kg/2), bytes 8*(kg%2)..+8.
+  const uint32_t frag_lane = (col & 15) + 16 * (kg >> 1);
+  const uint32_t nt_s = col >> 4;
+  const uint32_t half = kg & 1;
+  const uint32_t* colp = bsrc + col;
 
-  auto load_b = [&](v4i (&r)[kCopy], uint32_t ks) {
-    const v4i* p = bsrc + static_cast<size_t>(ks) * kFragsPerStep;
+  auto load_b = [&](uint32_t (&r)[8], uint32_t ks) {
 #pragma unroll
-    for (int j = 0; j < kCopy; ++j) r[j] = p[tid + kThreads * j];
+    for (int i = 0; i < 8; ++i) {
+      uint32_t k = ks * kBK + kg * 8 + i;
+      k = k < d_in ? k : d_in - 1;  // padded k: any in-bounds row (its weight digits are 0)
+      r[i] = colp[static_cast<size_t>(k) * bstride];
+    }
   };
-  auto store_b = [&](const v4i (&r)[kCopy], int buf) {
+  auto store_b = [&](const uint32_t (&r)[8], int buf) {
+    uint32_t lo[4], hi[4];
+    transpose4(r[0] + kBias, r[1] + kBias, r[2] + kBias, r[3] + kBias, lo);
+    transpose4(r[4] + kBias, r[5] + kBias, r[6] + kBias, r[7] + kBias, hi);
 #pragma unroll
-    for (int j = 0; j < kCopy; ++j) bs[buf][tid + kThreads * j] = r[j];
+    for (int b = 0; b < 4; ++b) {
+      uint2* dst = reinterpret_cast<uint2*>(&bs[buf][(nt_s * 4 + b) * 64 + frag_lane]) + half;
+      *dst = make_uint2(lo[b] ^ kBias, hi[b] ^ kBias);
+    }
   };
   auto load_a = [&](v4i (&a)[kMT][NDA], uint32_t ks) {
 #pragma unroll
@@ -171,10 +162,10 @@ __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint
       for (int d = 0; d < NDA; ++d)
         a[mt][d] = (adig_wave + ((static_cast<size_t>(mt) * ks_total + ks) * 4 + d) * 64)[lane];
   };
-  auto step = [&](uint32_t ks, v4i (&rb_issue)[kCopy], v4i (&rb_store)[kCopy]) {
+  auto step = [&](uint32_t ks, uint32_t (&r_issue)[8], const uint32_t (&r_store)[8]) {
     const int buf = ks & 1;
-    if (ks + 2 < ks_total) load_b(rb_issue, ks + 2);
-    if (ks + 1 < ks_total) load_a(a_nxt, ks + 1);
+    load_b(r_issue, ks + 2 < ks_total ? ks + 2 : ks_total - 1);
+    load_a(a_nxt, ks + 1 < ks_total ? ks + 1 : ks_total - 1);
     __builtin_amdgcn_sched_barrier(0);  // keep the prefetches ahead of the contractions
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
@@ -191,7 +182,7 @@ __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint
             acc[mt][nt][d + b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a_cur[mt][d], bf[nt], acc[mt][nt][d + b], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (ks + 1 < ks_total) store_b(rb_store, buf ^ 1);
+    store_b(r_store, buf ^ 1);
     __syncthreads();
 #pragma unroll
     for (int mt = 0; mt < kMT; ++mt)
@@ -199,17 +190,17 @@ __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint
       for (int d = 0; d < NDA; ++d) a_cur[mt][d] = a_nxt[mt][d];
   };
 
-  load_b(rb[0], 0);
-  if (ks_total > 1) load_b(rb[1], 1);
+  load_b(raw[0], 0);
+  load_b(raw[1], ks_total > 1 ? 1 : 0);
   load_a(a_cur, 0);
-  store_b(rb[0], 0);
+  store_b(raw[0], 0);
   __syncthreads();
   uint32_t ks = 0;
   for (; ks + 1 < ks_total; ks += 2) {
-    step(ks, rb[0], rb[1]);      // issues ks+2 into set 0, stores ks+1 from set 1
-    step(ks + 1, rb[1], rb[0]);  // issues ks+3 into set 1, stores ks+2 from set 0
+    step(ks, raw[0], raw[1]);      // issues ks+2 into set 0, converts ks+1 from set 1
+    step(ks + 1, raw[1], raw[0]);  // issues ks+3 into set 1, converts ks+2 from set 0
   }
-  if (ks < ks_total) step(ks, rb[0], rb[1]);
+  if (ks < ks_total) step(ks, raw[0], raw[1]);
 }
 
 // out = sum_s S_s 256^s mod q, exactly, in fp64 integer arithmetic.
@@ -264,19 +255,26 @@ __device__ __forceinline__ void epilogue(const v4i (&acc)[kMT][kNT][NDA + 3], co
 template <int NDA>
 __global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
     Tables tb, const v4i* __restrict__ adig, const uint32_t* __restrict__ flags,
-    const v4i* __restrict__ bdig, uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t limbs,
-    uint32_t mt_total, uint32_t ks_total, uint32_t tiles_m, uint32_t tiles_n) {
+    const uint32_t* __restrict__ ct_in, uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t d_in,
+    uint32_t limbs, uint32_t mt_total, uint32_t ks_total, uint32_t tiles_m, uint32_t tiles_n) {
   __shared__ v4i bs[2][kFragsPerStep];  // ciphertext digit fragments of one k-step, double buffered
 
-  // XCD-aware order: consecutive workgroup ids alternate XCDs; give each XCD a
-  // contiguous range of logical tiles (row tile fastest, then column, then limb).
+  // Tile order: consecutive workgroup ids alternate XCDs, so each XCD is given a
+  // contiguous range of logical tiles.  Logical order: limb, then groups of up
+  // to kGroupM row tiles (their weight digits, <= 1024 x d_in x 4 bytes, stay in
+  // the XCD's L2), then column tile, then row tile within the group.
   const uint32_t G = gridDim.x;
   uint32_t lid = blockIdx.x;
   if ((G & 7u) == 0) lid = (lid & 7u) * (G >> 3) + (lid >> 3);
-  const uint32_t mtile = lid % tiles_m;
-  lid /= tiles_m;
-  const uint32_t ntile = lid % tiles_n;
-  const uint32_t l = lid / tiles_n;
+  const uint32_t per_limb = tiles_m * tiles_n;
+  const uint32_t l = lid / per_limb;
+  uint32_t rem = lid - l * per_limb;
+  const uint32_t grp = rem / (kGroupM * tiles_n);           // full groups first
+  const uint32_t g0 = grp * kGroupM;
+  const uint32_t gsize = tiles_m - g0 < kGroupM ? tiles_m - g0 : kGroupM;
+  rem -= g0 * tiles_n;
+  const uint32_t ntile = rem / gsize;
+  const uint32_t mtile = g0 + rem % gsize;
 
   uint32_t top = 0;
 #pragma unroll
@@ -287,7 +285,8 @@ __global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const uint32_t col0 = ntile * kBN;  // column in [0, 2N): component c = col0 / N
   const uint32_t c = col0 >> tb.log_n, k0 = col0 & (n - 1);
-  const v4i* bsrc = bdig + (static_cast<size_t>(l) * tiles_n + ntile) * ks_total * kFragsPerStep;
+  const size_t bstride = 2ull * limbs * n;  // one input ciphertext
+  const uint32_t* bsrc = ct_in + (static_cast<size_t>(c) * limbs + l) * n + k0;
   const uint32_t mt_wave = mtile * (kBM / 16) + wave * kMT;
   const v4i* adig_wave = adig + (static_cast<size_t>(l) * mt_total + mt_wave) * ks_total * 4 * 64;
 
@@ -299,13 +298,13 @@ __global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
 #pragma unroll
       for (int s = 0; s < NDA + 3; ++s) acc[mt][nt][s] = v4i{0, 0, 0, 0};
 
-  mac_loop<NDA>(adig_wave, ks_total, bsrc, bs, acc);
+  mac_loop<NDA>(adig_wave, ks_total, bsrc, bstride, d_in, bs, acc);
   epilogue<NDA>(acc, tb, l, mt_wave, lane, d_out, c, limbs, k0, ct_out);
 }
 
 struct Shape {
   uint32_t tiles_m, tiles_n, mt_total, ks_total;
-  size_t adig_bytes, flag_bytes, bdig_bytes;
+  size_t adig_bytes, flag_bytes;
 };
 
 Shape shape_of(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
@@ -316,7 +315,6 @@ Shape shape_of(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
   s.ks_total = (d_in + kBK - 1) / kBK;
   s.adig_bytes = static_cast<size_t>(limbs) * s.mt_total * s.ks_total * 4 * 64 * sizeof(v4i);
   s.flag_bytes = ((static_cast<size_t>(limbs) * s.mt_total * 4) + 255) & ~size_t(255);
-  s.bdig_bytes = static_cast<size_t>(limbs) * s.tiles_n * s.ks_total * kFragsPerStep * sizeof(v4i);
   return s;
 }
 
@@ -325,7 +323,7 @@ Shape shape_of(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
 size_t mac_mfma_workspace_bytes(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
   if (d_out == 0 || d_in == 0 || d_in > kMaxDin) return 0;
   const Shape s = shape_of(n, d_out, d_in, limbs);
-  return s.adig_bytes + s.flag_bytes + s.bdig_bytes;
+  return s.adig_bytes + s.flag_bytes;
 }
 
 bool mac_mfma_supported(uint32_t d_in) { return d_in >= 1 && d_in <= kMaxDin; }
@@ -337,17 +335,13 @@ hipError_t launch_mac_scalar_mfma(const Tables& t, const uint32_t* w_enc, const 
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   v4i* adig = reinterpret_cast<v4i*>(ws);
   uint32_t* flags = reinterpret_cast<uint32_t*>(ws + s.adig_bytes);
-  v4i* bdig = reinterpret_cast<v4i*>(ws + s.adig_bytes + s.flag_bytes);
   mfma_prep_kernel<<<dim3(s.mt_total, limbs), kThreads, 0, st>>>(t.q, w_enc, d_out, d_in, limbs, s.mt_total,
                                                                  s.ks_total, adig, flags);
-  const size_t bgrid = static_cast<size_t>(limbs) * s.tiles_n * s.ks_total;
-  mfma_bprep_kernel<<<static_cast<uint32_t>(bgrid), kBprepThreads, 0, st>>>(ct_in, d_in, limbs, t.log_n, s.tiles_n,
-                                                                      s.ks_total, bdig);
   const size_t grid = static_cast<size_t>(limbs) * s.tiles_n * s.tiles_m;
-  mac_mfma_kernel<3><<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, bdig, ct_out, d_out, limbs,
-                                                                      s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
-  mac_mfma_kernel<4><<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, bdig, ct_out, d_out, limbs,
-                                                                      s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
+  mac_mfma_kernel<3><<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, ct_in, ct_out, d_out, d_in,
+                                                                      limbs, s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
+  mac_mfma_kernel<4><<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, ct_in, ct_out, d_out, d_in,
+                                                                      limbs, s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
   return hipGetLastError();
 }
 
