@@ -327,11 +327,19 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
     delete c;
     return hip_fail(he, "hipMemcpy(context tables)");
   }
+  int cus = 0;
+  he = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+  if (he != hipSuccess || cus <= 0) {
+    (void)hipFree(c->dev);
+    delete c;
+    return hip_fail(he == hipSuccess ? hipErrorInvalidDevice : he, "hipDeviceGetAttribute(compute units)");
+  }
   auto* base = static_cast<unsigned char*>(c->dev);
   ckks::Tables& t = c->t;
   t.log_n = log_n;
   t.n = n;
   t.L = L;
+  t.num_cus = static_cast<uint32_t>(cus);
   t.q = reinterpret_cast<const uint32_t*>(base + o_q);
   t.fwd = reinterpret_cast<const uint32_t*>(base + o_fwd);
   t.fwd_shoup = reinterpret_cast<const uint32_t*>(base + o_fwds);

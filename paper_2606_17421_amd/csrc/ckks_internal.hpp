@@ -19,6 +19,7 @@ struct Tables {
   uint32_t log_n;
   uint32_t n;
   uint32_t L;
+  uint32_t num_cus;            // compute units of the context's device
   const uint32_t* q;           // [L]
   const uint32_t* fwd;         // [L][N]  psi_l^brv(k)         (forward twiddles)
   const uint32_t* fwd_shoup;   // [L][N]  floor(fwd * 2^32 / q)

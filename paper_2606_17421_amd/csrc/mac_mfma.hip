@@ -49,6 +49,8 @@ constexpr int kFragsPerStep = kNT * 4 * 64;  // 16-byte ciphertext fragments per
 constexpr int kGroupM = 8;                   // row tiles per L2-resident weight group
 constexpr uint32_t kBias = 0x80808080u;
 constexpr uint32_t kMaxDin = 4096;
+constexpr int kRsrcWord3 = 0x00020000;  // buffer resource word 3: 32-bit raw data, range-checked
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 
 // o[b] byte e = p[e] byte b (4x4 byte transpose, eight v_perm_b32).
@@ -121,7 +123,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(
 // buffer (ks+1)%2; synchronise once.
 template <int NDA>
 __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint32_t ks_total,
-                                         const uint32_t* __restrict__ bsrc, size_t bstride,
+                                         const uint32_t* __restrict__ bsrc, uint32_t row_bytes,
                                          uint32_t d_in, v4i (*bs)[kFragsPerStep],
                                          v4i (&acc)[kMT][kNT][NDA + 3]) {
   const uint32_t tid = threadIdx.x;
@@ -129,21 +131,24 @@ __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint
   const uint32_t col = tid % kBN;       // staging: column of the tile
   const uint32_t kg = tid / kBN;        // staging: 8-k group within the step (0..7)
   uint32_t raw[2][8];
-  v4i a_cur[kMT][NDA], a_nxt[kMT][NDA];
+  v4i af[2][kMT][NDA];
   // LDS byte offset of this thread's 8 bytes of digit-b fragment: fragment
   // (nt, b), MFMA lane col%16 + 16*(kg/2), bytes 8*(kg%2)..+8.
   const uint32_t frag_lane = (col & 15) + 16 * (kg >> 1);
   const uint32_t nt_s = col >> 4;
   const uint32_t half = kg & 1;
-  const uint32_t* colp = bsrc + col;
-
-  auto load_b = [&](uint32_t (&r)[8], uint32_t ks) {
+  uint32_t voff[8];  // byte offset of (row kg*8+i, this column) from the step's first row
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      uint32_t k = ks * kBK + kg * 8 + i;
-      k = k < d_in ? k : d_in - 1;  // padded k: any in-bounds row (its weight digits are 0)
-      r[i] = colp[static_cast<size_t>(k) * bstride];
-    }
+  for (int i = 0; i < 8; ++i) voff[i] = (kg * 8 + i) * row_bytes + col * 4;
+  const uint32_t row_words = row_bytes >> 2;
+
+  // Rows at or past d_in fall outside the step's buffer range and read as 0.
+  auto load_b = [&](uint32_t (&r)[8], uint32_t ks) {
+    const uint32_t rows = d_in - ks * kBK < kBK ? d_in - ks * kBK : kBK;
+    const rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint32_t*>(bsrc) + static_cast<size_t>(ks) * kBK * row_words, 0, rows * row_bytes, kRsrcWord3);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff[i], 0, 0);
   };
   auto store_b = [&](const uint32_t (&r)[8], int buf) {
     uint32_t lo[4], hi[4];
@@ -155,14 +160,17 @@ __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint
       *dst = make_uint2(lo[b] ^ kBias, hi[b] ^ kBias);
     }
   };
+  const rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<v4i*>(adig_wave), 0,
+                                                      kMT * ks_total * 4 * 64 * 16, kRsrcWord3);
   auto load_a = [&](v4i (&a)[kMT][NDA], uint32_t ks) {
 #pragma unroll
     for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
       for (int d = 0; d < NDA; ++d)
-        a[mt][d] = (adig_wave + ((static_cast<size_t>(mt) * ks_total + ks) * 4 + d) * 64)[lane];
+        a[mt][d] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(ra, lane * 16, ((mt * ks_total + ks) * 4 + d) * 1024, 0);
   };
-  auto step = [&](uint32_t ks, uint32_t (&r_issue)[8], const uint32_t (&r_store)[8]) {
+  auto step = [&](uint32_t ks, uint32_t (&r_issue)[8], const uint32_t (&r_store)[8], v4i (&a_cur)[kMT][NDA],
+                  v4i (&a_nxt)[kMT][NDA]) {
     const int buf = ks & 1;
     load_b(r_issue, ks + 2 < ks_total ? ks + 2 : ks_total - 1);
     load_a(a_nxt, ks + 1 < ks_total ? ks + 1 : ks_total - 1);
@@ -184,67 +192,55 @@ __device__ __forceinline__ void mac_loop(const v4i* __restrict__ adig_wave, uint
     __builtin_amdgcn_sched_barrier(0);
     store_b(r_store, buf ^ 1);
     __syncthreads();
-#pragma unroll
-    for (int mt = 0; mt < kMT; ++mt)
-#pragma unroll
-      for (int d = 0; d < NDA; ++d) a_cur[mt][d] = a_nxt[mt][d];
   };
 
   load_b(raw[0], 0);
   load_b(raw[1], ks_total > 1 ? 1 : 0);
-  load_a(a_cur, 0);
+  load_a(af[0], 0);
   store_b(raw[0], 0);
   __syncthreads();
   uint32_t ks = 0;
   for (; ks + 1 < ks_total; ks += 2) {
-    step(ks, raw[0], raw[1]);      // issues ks+2 into set 0, converts ks+1 from set 1
-    step(ks + 1, raw[1], raw[0]);  // issues ks+3 into set 1, converts ks+2 from set 0
+    step(ks, raw[0], raw[1], af[0], af[1]);      // issues ks+2 into set 0, converts ks+1 from set 1
+    step(ks + 1, raw[1], raw[0], af[1], af[0]);  // issues ks+3 into set 1, converts ks+2 from set 0
   }
-  if (ks < ks_total) step(ks, raw[0], raw[1]);
+  if (ks < ks_total) step(ks, raw[0], raw[1], af[0], af[1]);
 }
 
-// out = sum_s S_s 256^s mod q, exactly, in fp64 integer arithmetic.
+// out = sum_s S_s 256^s mod q, exactly.  T = sum_{s<4} S_s 2^(8s) +
+// sum_{s>=4} S_s (256^s mod q) is an exact signed 64-bit sum (|T| < 2^59.7 for
+// |S_s| <= 2^28 and q < 2^30).  The quotient estimate floor(T / q) from fp64
+// (T rounded once, then times 1/q) is within one of the true quotient and below
+// 2^31 in magnitude (q > 2^29), so r = T - qt q lies in [-q, 2q) and its low 32
+// bits are exact; r + q in [0, 3q) then takes two conditional subtractions.
 template <int NDA>
 __device__ __forceinline__ void epilogue(const v4i (&acc)[kMT][kNT][NDA + 3], const Tables& tb, uint32_t l,
-                                         uint32_t mt_wave, uint32_t lane, uint32_t d_out, uint32_t c,
-                                         uint32_t limbs, uint32_t k0, uint32_t* __restrict__ ct_out) {
-  const uint32_t n = tb.n;
-  const uint32_t qi = tb.q[l];
-  const double q = static_cast<double>(qi);
+                                         uint32_t lane, const rsrc_t& out, uint32_t row_bytes) {
+  const uint32_t q = tb.q[l];
   const double qr = tb.q_recip[l];
   const uint32_t* pw = tb.pow256 + l * 8;
-  const double c4h = static_cast<double>(pw[4] >> 15), c4l = static_cast<double>(pw[4] & 0x7fffu);
-  const double c5h = static_cast<double>(pw[5] >> 15), c5l = static_cast<double>(pw[5] & 0x7fffu);
-  const double c6h = static_cast<double>(pw[6] >> 15), c6l = static_cast<double>(pw[6] & 0x7fffu);
+  // 256^s mod q as signed multipliers (2^(8s) itself for s < 4, since 2^24 < q)
+  int32_t cs[NDA + 3];
+#pragma unroll
+  for (int s = 1; s < NDA + 3; ++s) cs[s] = static_cast<int32_t>(pw[s]);
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const uint32_t j = (mt_wave + mt) * 16 + 4 * (lane >> 4) + r;
-      if (j >= d_out) continue;
-      uint32_t* orow = ct_out + ((static_cast<size_t>(j) * 2 + c) * limbs + l) * n + k0 + (lane & 15);
+      // output row mt*16 + 4*(lane/16) + r of the wave; rows past d_out are out of range
+      const uint32_t voff = (mt * 16 + 4 * (lane >> 4) + r) * row_bytes + (lane & 15) * 4;
 #pragma unroll
       for (int nt = 0; nt < kNT; ++nt) {
         const v4i* a = acc[mt][nt];
-        // classes 0..3: exact (|sum| < 2^52.01)
-        const double vlo = fma(static_cast<double>(a[3][r]), 16777216.0,
-                               fma(static_cast<double>(a[2][r]), 65536.0,
-                                   fma(static_cast<double>(a[1][r]), 256.0, static_cast<double>(a[0][r]))));
-        // classes 4..6 with 256^s mod q = ch 2^15 + cl (each partial sum < 2^45, exact)
-        const double a4 = static_cast<double>(a[4][r]), a5 = static_cast<double>(a[5][r]);
-        double th = fma(a5, c5h, a4 * c4h);
-        double tl = fma(a5, c5l, a4 * c4l);
-        if constexpr (NDA == 4) {
-          const double a6 = static_cast<double>(a[6][r]);
-          th = fma(a6, c6h, th);
-          tl = fma(a6, c6l, tl);
-        }
-        const double rh = fma(-floor(th * qr), q, th);         // th mod q, in (-q, 2q)
-        const double v = fma(rh, 32768.0, vlo + tl);            // |v| < 2^52.2, exact
-        double rem = fma(-floor(v * qr), q, v);                 // in [-q, 2q)
-        rem += rem < 0.0 ? q : 0.0;
-        rem -= rem >= q ? q : 0.0;
-        orow[nt * 16] = static_cast<uint32_t>(rem);
+        int64_t t = a[0][r];
+#pragma unroll
+        for (int s = 1; s < NDA + 3; ++s) t += static_cast<int64_t>(a[s][r]) * static_cast<int64_t>(cs[s]);
+        const double tf = static_cast<double>(t);
+        const int32_t qt = static_cast<int32_t>(floor(tf * qr));
+        uint32_t u = static_cast<uint32_t>(t) - static_cast<uint32_t>(qt) * q + q;  // r + q, in [0, 3q)
+        u = min(u, u - q);
+        u = min(u, u - q);
+        __builtin_amdgcn_raw_buffer_store_b32(u, out, voff, nt * 64, 0);
       }
     }
   }
@@ -285,7 +281,7 @@ __global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const uint32_t col0 = ntile * kBN;  // column in [0, 2N): component c = col0 / N
   const uint32_t c = col0 >> tb.log_n, k0 = col0 & (n - 1);
-  const size_t bstride = 2ull * limbs * n;  // one input ciphertext
+  const uint32_t row_bytes = 2u * limbs * n * 4u;  // one input ciphertext
   const uint32_t* bsrc = ct_in + (static_cast<size_t>(c) * limbs + l) * n + k0;
   const uint32_t mt_wave = mtile * (kBM / 16) + wave * kMT;
   const v4i* adig_wave = adig + (static_cast<size_t>(l) * mt_total + mt_wave) * ks_total * 4 * 64;
@@ -298,8 +294,13 @@ __global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
 #pragma unroll
       for (int s = 0; s < NDA + 3; ++s) acc[mt][nt][s] = v4i{0, 0, 0, 0};
 
-  mac_loop<NDA>(adig_wave, ks_total, bsrc, bstride, d_in, bs, acc);
-  epilogue<NDA>(acc, tb, l, mt_wave, lane, d_out, c, limbs, k0, ct_out);
+  mac_loop<NDA>(adig_wave, ks_total, bsrc, row_bytes, d_in, bs, acc);
+  const uint32_t row0 = mt_wave * 16;
+  const uint32_t row_bytes_out = 2u * limbs * n * 4u;
+  const uint32_t rows = row0 < d_out ? (d_out - row0 < kMT * 16 ? d_out - row0 : kMT * 16) : 0;
+  uint32_t* dst = ct_out + ((static_cast<size_t>(row0) * 2 + c) * limbs + l) * n + k0;
+  const rsrc_t out = __builtin_amdgcn_make_buffer_rsrc(dst, 0, rows * row_bytes_out, kRsrcWord3);
+  epilogue<NDA>(acc, tb, l, lane, out, row_bytes_out);
 }
 
 struct Shape {
