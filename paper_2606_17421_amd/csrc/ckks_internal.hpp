@@ -49,6 +49,13 @@ __device__ __forceinline__ uint32_t mul_shoup(uint32_t a, uint32_t w, uint32_t w
   return min(r, r - q);
 }
 
+// Lazy Shoup product: any a < 2^32, w < q, ws = floor(w 2^32 / q).  The
+// quotient estimate floor(a ws / 2^32) is within one of floor(a w / q), so the
+// result lies in [0, 2q).
+__device__ __forceinline__ uint32_t mul_shoup_lazy(uint32_t a, uint32_t w, uint32_t ws, uint32_t q) {
+  return a * w - __umulhi(a, ws) * q;
+}
+
 __device__ __forceinline__ uint32_t add_mod(uint32_t a, uint32_t b, uint32_t q) {
   uint32_t s = a + b;
   return min(s, s - q);

@@ -8,7 +8,11 @@
 // A transform (or a 2^LOGB-point block of one) is split into groups of LOGE
 // consecutive index bits.  For one group a thread owns E = 2^LOGE residues
 // whose indices differ only in the group's window of bits, and runs all the
-// group's stages in registers (a radix-E butterfly network).  Between groups
+// group's stages in registers (a radix-E butterfly network).  Butterflies are
+// lazy (Harvey): forward values stay in [0, 4q) and inverse values in [0, 2q)
+// (4q < 2^32 for q < 2^30), and a block normalises to [0, q) when it ends; a
+// forward group run on its own (the N = 2^16 column pass) leaves [0, 4q),
+// which the next forward stage accepts.  Between groups
 // the residues are exchanged through LDS, padded by one word per 32 so that
 // power-of-two strides spread across banks.  Group 0 covers the top bits, so
 // its window is a stride-T pattern (coalesced HBM access) and the last group's
@@ -48,6 +52,7 @@ __device__ __forceinline__ void fwd_group(uint32_t (&v)[1 << LOGE], uint32_t t, 
                                           const uint32_t* __restrict__ tws, uint32_t q) {
   using P = Plan<LOGB, LOGE>;
   constexpr int w = P::lo(G);
+  const uint32_t q2 = 2 * q;
 #pragma unroll
   for (int b = P::hi(G); b >= P::lo(G); --b) {
     const int s = LOGN - 1 - b;
@@ -62,10 +67,11 @@ __device__ __forceinline__ void fwd_group(uint32_t (&v)[1 << LOGE], uint32_t t, 
       for (int low = 0; low < (1 << lb); ++low) {
         const int j0 = (u << (lb + 1)) | low;
         const int j1 = j0 | (1 << lb);
-        const uint32_t U = v[j0];
-        const uint32_t V = mul_shoup(v[j1], wv, wsv, q);
-        v[j0] = add_mod(U, V, q);
-        v[j1] = sub_mod(U, V, q);
+        uint32_t U = v[j0];
+        U = min(U, U - q2);                               // [0, 2q)
+        const uint32_t V = mul_shoup_lazy(v[j1], wv, wsv, q);  // [0, 2q)
+        v[j0] = U + V;                                    // [0, 4q)
+        v[j1] = U - V + q2;                               // (0, 4q)
       }
     }
   }
@@ -78,6 +84,7 @@ __device__ __forceinline__ void inv_group(uint32_t (&v)[1 << LOGE], uint32_t t, 
                                           const uint32_t* __restrict__ tws, uint32_t q) {
   using P = Plan<LOGB, LOGE>;
   constexpr int w = P::lo(G);
+  const uint32_t q2 = 2 * q;
 #pragma unroll
   for (int b = P::lo(G); b <= P::hi(G); ++b) {
     const int s = LOGN - 1 - b;
@@ -92,10 +99,10 @@ __device__ __forceinline__ void inv_group(uint32_t (&v)[1 << LOGE], uint32_t t, 
       for (int low = 0; low < (1 << lb); ++low) {
         const int j0 = (u << (lb + 1)) | low;
         const int j1 = j0 | (1 << lb);
-        const uint32_t U = v[j0];
-        const uint32_t V = v[j1];
-        v[j0] = add_mod(U, V, q);
-        v[j1] = mul_shoup(sub_mod(U, V, q), wv, wsv, q);
+        const uint32_t U = v[j0], V = v[j1];
+        const uint32_t S = U + V;                         // [0, 4q)
+        v[j0] = min(S, S - q2);                           // [0, 2q)
+        v[j1] = mul_shoup_lazy(U - V + q2, wv, wsv, q);   // [0, 2q)
       }
     }
   }
@@ -123,7 +130,15 @@ __device__ __forceinline__ void fwd_block(uint32_t (&v)[1 << LOGE], uint32_t t, 
   using P = Plan<LOGB, LOGE>;
   if constexpr (G > 0) exchange<LOGB, LOGE, G - 1, G>(v, t, lds);
   fwd_group<LOGN, LOGB, LOGE, G>(v, t, blk, tw, tws, q);
-  if constexpr (G + 1 < P::NG) fwd_block<LOGN, LOGB, LOGE, G + 1>(v, t, blk, tw, tws, q, lds);
+  if constexpr (G + 1 < P::NG) {
+    fwd_block<LOGN, LOGB, LOGE, G + 1>(v, t, blk, tw, tws, q, lds);
+  } else {
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) {  // [0, 4q) -> [0, q)
+      uint32_t x = min(v[j], v[j] - 2 * q);
+      v[j] = min(x, x - q);
+    }
+  }
 }
 
 // Inverse transform (without the N^-1 factor) of one block held in group
@@ -136,7 +151,12 @@ __device__ __forceinline__ void inv_block(uint32_t (&v)[1 << LOGE], uint32_t t, 
   using P = Plan<LOGB, LOGE>;
   if constexpr (G < P::NG - 1) exchange<LOGB, LOGE, G + 1, G>(v, t, lds);
   inv_group<LOGN, LOGB, LOGE, G>(v, t, blk, tw, tws, q);
-  if constexpr (G > 0) inv_block<LOGN, LOGB, LOGE, G - 1>(v, t, blk, tw, tws, q, lds);
+  if constexpr (G > 0) {
+    inv_block<LOGN, LOGB, LOGE, G - 1>(v, t, blk, tw, tws, q, lds);
+  } else {
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = min(v[j], v[j] - q);  // [0, 2q) -> [0, q)
+  }
 }
 
 // Per-N choice of residues per thread for whole-polynomial blocks.
