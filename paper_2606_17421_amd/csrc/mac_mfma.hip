@@ -11,27 +11,24 @@
 // Then  sum_i v_i x_i = sum_s 256^s S_s,  S_s = sum_{a+b=s} sum_i e_a(i) d_b(i),
 // where each S_s is an exact i32 contraction on v_mfma_i32_16x16x64_i8
 // (|S_s| <= 4 * d_in * 2^14 <= 2^28 for d_in <= 4096).  The epilogue folds the
-// classes with exact fp64 integer arithmetic: classes 0..3 with their weights
-// 2^(8s) (a sum below 2^52.01), classes 4..6 with 256^s mod q split into 15-bit
-// halves, one intermediate reduction, then one final reduction mod q.
+// classes exactly in signed 64-bit integers, with 256^s mod q for s >= 4, and
+// reduces the sum mod q through one fp64 quotient estimate.
 // Digit products: 12 per modular MAC with 3 weight digits, 16 with 4.
 //
-// Two prep kernels lay both operands out as MFMA fragments (16 bytes per lane,
-// the lane order of v_mfma_i32_16x16x64_i8): the weights per 16-row tile (with
-// a flag for tiles that need a fourth digit), the ciphertext residues per
-// 64-column tile and 64-deep k-step.  The residue conversion is a streaming
-// pass (read 4 B, write 4 B per residue) done once, instead of once per row
-// tile inside the contraction.
+// A prep kernel lays the weights out as MFMA fragments (16 bytes per lane, the
+// lane order of v_mfma_i32_16x16x64_i8) per 16-row tile and 64-deep k-step,
+// with a flag for tiles that need a fourth digit.
 //
-// Contraction: a 256-thread workgroup computes a 128 (rows) x 64 (columns)
-// tile of one limb; each wave owns 32 rows x 64 columns (2 x 4 MFMA tiles x 6
-// or 7 shift-class accumulators in AGPRs).  Per 64-deep k-step the workgroup
-// copies the 16 KiB of ciphertext digit fragments into an LDS double buffer
-// (loads issued two steps ahead) and each wave reads its weight fragments
-// from global memory (L2 resident; issued one step ahead).  Workgroups are
-// ordered (limb, column tile, row tile) with row tiles fastest and remapped so
-// that each XCD runs a contiguous range: tiles sharing a column tile, and a
-// whole limb's weights, stay in one XCD's L2.
+// Contraction: a 256-thread workgroup computes a 128 (rows) x 32 (columns)
+// tile of one limb; each wave owns 32 rows x 32 columns (2 x 2 MFMA tiles x 6
+// or 7 shift-class accumulators).  Per k-step the workgroup converts the raw
+// residues of its 32 columns (raw buffer loads issued two steps ahead; rows
+// past d_in read as zero through the buffer range check) into digit fragments
+// in an LDS double buffer, and each wave reads its weight fragments from
+// global memory (L2 resident, issued one step ahead).  Workgroups run in an
+// XCD-aware grouped order so that the weights of a row group and the columns
+// shared by its row tiles stay in one XCD's L2.  One workgroup-uniform branch
+// per tile selects three or four weight digits.
 #include "ckks_internal.hpp"
 
 namespace ckks {
@@ -246,9 +243,23 @@ __device__ __forceinline__ void epilogue(const v4i (&acc)[kMT][kNT][NDA + 3], co
   }
 }
 
-// One instantiation per weight-digit count; both are launched over the full
-// grid and a workgroup exits at once unless its row tile's flag selects it.
+// One workgroup-uniform branch per row tile: tiles whose weights need a fourth
+// digit (flag set) take the NDA = 4 contraction, the others NDA = 3.
 template <int NDA>
+__device__ __forceinline__ void mac_tile(const Tables& tb, const v4i* __restrict__ adig_wave, uint32_t ks_total,
+                                         const uint32_t* __restrict__ bsrc, uint32_t row_bytes, uint32_t d_in,
+                                         v4i (*bs)[kFragsPerStep], const rsrc_t& out, uint32_t l, uint32_t lane) {
+  v4i acc[kMT][kNT][NDA + 3];
+#pragma unroll
+  for (int mt = 0; mt < kMT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt)
+#pragma unroll
+      for (int s = 0; s < NDA + 3; ++s) acc[mt][nt][s] = v4i{0, 0, 0, 0};
+  mac_loop<NDA>(adig_wave, ks_total, bsrc, row_bytes, d_in, bs, acc);
+  epilogue<NDA>(acc, tb, l, lane, out, row_bytes);
+}
+
 __global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
     Tables tb, const v4i* __restrict__ adig, const uint32_t* __restrict__ flags,
     const uint32_t* __restrict__ ct_in, uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t d_in,
@@ -275,32 +286,23 @@ __global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
   uint32_t top = 0;
 #pragma unroll
   for (int i = 0; i < kBM / 16; ++i) top |= flags[l * mt_total + mtile * (kBM / 16) + i];
-  if ((top != 0) != (NDA == 4)) return;  // workgroup-uniform
 
   const uint32_t n = tb.n;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const uint32_t col0 = ntile * kBN;  // column in [0, 2N): component c = col0 / N
   const uint32_t c = col0 >> tb.log_n, k0 = col0 & (n - 1);
-  const uint32_t row_bytes = 2u * limbs * n * 4u;  // one input ciphertext
+  const uint32_t row_bytes = 2u * limbs * n * 4u;  // one ciphertext, input and output alike
   const uint32_t* bsrc = ct_in + (static_cast<size_t>(c) * limbs + l) * n + k0;
   const uint32_t mt_wave = mtile * (kBM / 16) + wave * kMT;
   const v4i* adig_wave = adig + (static_cast<size_t>(l) * mt_total + mt_wave) * ks_total * 4 * 64;
-
-  v4i acc[kMT][kNT][NDA + 3];
-#pragma unroll
-  for (int mt = 0; mt < kMT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < kNT; ++nt)
-#pragma unroll
-      for (int s = 0; s < NDA + 3; ++s) acc[mt][nt][s] = v4i{0, 0, 0, 0};
-
-  mac_loop<NDA>(adig_wave, ks_total, bsrc, row_bytes, d_in, bs, acc);
   const uint32_t row0 = mt_wave * 16;
-  const uint32_t row_bytes_out = 2u * limbs * n * 4u;
   const uint32_t rows = row0 < d_out ? (d_out - row0 < kMT * 16 ? d_out - row0 : kMT * 16) : 0;
   uint32_t* dst = ct_out + ((static_cast<size_t>(row0) * 2 + c) * limbs + l) * n + k0;
-  const rsrc_t out = __builtin_amdgcn_make_buffer_rsrc(dst, 0, rows * row_bytes_out, kRsrcWord3);
-  epilogue<NDA>(acc, tb, l, lane, out, row_bytes_out);
+  const rsrc_t out = __builtin_amdgcn_make_buffer_rsrc(dst, 0, rows * row_bytes, kRsrcWord3);
+  if (top != 0)
+    mac_tile<4>(tb, adig_wave, ks_total, bsrc, row_bytes, d_in, bs, out, l, lane);
+  else
+    mac_tile<3>(tb, adig_wave, ks_total, bsrc, row_bytes, d_in, bs, out, l, lane);
 }
 
 struct Shape {
@@ -339,10 +341,9 @@ hipError_t launch_mac_scalar_mfma(const Tables& t, const uint32_t* w_enc, const 
   mfma_prep_kernel<<<dim3(s.mt_total, limbs), kThreads, 0, st>>>(t.q, w_enc, d_out, d_in, limbs, s.mt_total,
                                                                  s.ks_total, adig, flags);
   const size_t grid = static_cast<size_t>(limbs) * s.tiles_n * s.tiles_m;
-  mac_mfma_kernel<3><<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, ct_in, ct_out, d_out, d_in,
-                                                                      limbs, s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
-  mac_mfma_kernel<4><<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, ct_in, ct_out, d_out, d_in,
-                                                                      limbs, s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
+  if (grid >= (size_t(1) << 31)) return hipErrorInvalidValue;  // tile indices are 32-bit
+  mac_mfma_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, ct_in, ct_out, d_out, d_in, limbs,
+                                                                   s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
   return hipGetLastError();
 }
 
