@@ -12,7 +12,7 @@ namespace ckks {
 namespace {
 
 template <int LOGN, bool INV>
-__global__ __launch_bounds__(WholePlan<LOGN>::P::T) void ntt_whole_kernel(Tables tb, uint32_t* rows,
+__global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSimd) void ntt_whole_kernel(Tables tb, uint32_t* rows,
                                                                           uint32_t limbs) {
   using P = typename WholePlan<LOGN>::P;
   constexpr int LOGE = WholePlan<LOGN>::LOGE;

@@ -109,15 +109,35 @@ __device__ __forceinline__ void inv_group(uint32_t (&v)[1 << LOGE], uint32_t t, 
 }
 
 // Move the thread's residues from group GF's layout to group GT's through LDS.
+// When both groups keep at most 6 low index bits in the thread id (lo(g) <= 6),
+// the 64 threads of a wave hold the same index set in both layouts (all
+// indices whose bits from LOGE + 6 up equal the wave number), so the exchange
+// stays inside the wave's own LDS region: no workgroup barrier, only the
+// wave's in-order LDS accesses (wave_barrier keeps the compiler from moving
+// them).  Any other exchange is workgroup-wide and synchronises; it also
+// orders every earlier wave-local access before its writes.
 template <int LOGB, int LOGE, int GF, int GT>
 __device__ __forceinline__ void exchange(uint32_t (&v)[1 << LOGE], uint32_t t, uint32_t* lds) {
   using P = Plan<LOGB, LOGE>;
-  __syncthreads();  // earlier readers of lds are done
+  constexpr bool wave_local = P::lo(GF) <= 6 && P::lo(GT) <= 6;
+  if constexpr (wave_local) {
+    __builtin_amdgcn_wave_barrier();
+  } else {
+    __syncthreads();  // earlier readers of lds are done
+  }
+  // t's bits and j's bits of a position are disjoint, so the padded position
+  // splits into a per-thread base and a compile-time offset per j.
+  uint32_t* wb = lds + lds_pad(P::template pos<GF>(t, 0));
 #pragma unroll
-  for (int j = 0; j < P::E; ++j) lds[lds_pad(P::template pos<GF>(t, j))] = v[j];
-  __syncthreads();
+  for (int j = 0; j < P::E; ++j) wb[lds_pad(P::template pos<GF>(0, j))] = v[j];
+  if constexpr (wave_local) {
+    __builtin_amdgcn_wave_barrier();
+  } else {
+    __syncthreads();
+  }
+  const uint32_t* rb = lds + lds_pad(P::template pos<GT>(t, 0));
 #pragma unroll
-  for (int j = 0; j < P::E; ++j) v[j] = lds[lds_pad(P::template pos<GT>(t, j))];
+  for (int j = 0; j < P::E; ++j) v[j] = rb[lds_pad(P::template pos<GT>(0, j))];
 }
 
 // Forward transform of one block held in registers in group-0 layout; on
@@ -159,11 +179,14 @@ __device__ __forceinline__ void inv_block(uint32_t (&v)[1 << LOGE], uint32_t t, 
   }
 }
 
-// Per-N choice of residues per thread for whole-polynomial blocks.
+// Per-N choice of residues per thread for whole-polynomial blocks.  Kernels
+// over whole polynomials ask for 4 waves per SIMD (a 128-register budget):
+// two 2^14 workgroups, or one 2^15 workgroup, fill a CU's LDS.
 template <int LOGN>
 struct WholePlan {
   static constexpr int LOGE = LOGN <= 12 ? 4 : 5;
   using P = Plan<LOGN, LOGE>;
+  static constexpr int kWavesPerSimd = 4;
 };
 
 }  // namespace ckks

@@ -16,7 +16,7 @@ namespace ckks {
 namespace {
 
 template <int LOGN>
-__global__ __launch_bounds__(WholePlan<LOGN>::P::T) void rescale_kernel(
+__global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSimd) void rescale_kernel(
     Tables tb, const uint32_t* __restrict__ in, uint32_t* __restrict__ out, uint32_t limbs) {
   using P = typename WholePlan<LOGN>::P;
   constexpr int LOGE = WholePlan<LOGN>::LOGE;
