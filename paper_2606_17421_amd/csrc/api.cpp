@@ -528,7 +528,7 @@ int ckks_rescale(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t* ct_out, u
   if (count > 0x3FFFFFFFu) return fail(CKKS_E_INVALID_ARG, "count=%u too large", count);
   if (int rc = check_ptr(ct_in, "ct_in")) return rc;
   if (int rc = check_ptr(ct_out, "ct_out")) return rc;
-  const size_t need = ckks::rescale_workspace_bytes(ctx->t, count);
+  const size_t need = ckks::rescale_workspace_bytes(ctx->t, count, limbs);
   if (need && (!workspace || workspace_bytes < need))
     return fail(CKKS_E_WORKSPACE, "rescale workspace %zu bytes < %zu required", workspace_bytes, need);
   if (need && !aligned16(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 16-byte aligned");
@@ -544,7 +544,7 @@ size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b,
     case CKKS_OP_MAC_SCALAR:
       return ctx->mac_algo == CKKS_MAC_VALU ? 0 : ckks::mac_mfma_workspace_bytes(ctx->n, a, b, limbs);
     case CKKS_OP_RESCALE:
-      return limbs < 2 ? static_cast<size_t>(-1) : ckks::rescale_workspace_bytes(ctx->t, a);
+      return limbs < 2 ? static_cast<size_t>(-1) : ckks::rescale_workspace_bytes(ctx->t, a, limbs);
     case CKKS_OP_ENCODE_POLY:
       return 0;
     default:

@@ -121,7 +121,7 @@ hipError_t launch_mac_poly(const Tables& t, const uint32_t* pt, const uint32_t* 
                            uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
                            hipStream_t s);
 
-size_t rescale_workspace_bytes(const Tables& t, uint32_t count);
+size_t rescale_workspace_bytes(const Tables& t, uint32_t count, uint32_t limbs);
 hipError_t launch_rescale(const Tables& t, const uint32_t* ct_in, uint32_t* ct_out, uint32_t count,
                           uint32_t limbs, void* workspace, hipStream_t s);
 

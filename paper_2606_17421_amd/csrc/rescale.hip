@@ -9,7 +9,7 @@
 // transform's starting layout) while each remaining limb is forward-
 // transformed and combined with c_l on the way out.  HBM traffic is the
 // minimum: read limbs rows, write limbs - 1 rows.
-// N = 2^16: staged through a workspace with the two-pass NTT.
+// N = 2^16: three passes through a workspace (see below).
 #include "ntt_core.hpp"
 
 namespace ckks {
@@ -57,91 +57,128 @@ __global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSi
   }
 }
 
-// ---- N = 2^16 staging kernels (rows of 2^16 residues) ----------------------
-constexpr int kT = 256;
+// ---- N = 2^16: three passes over a chunk of polynomials --------------------
+// A row of 2^16 residues (256 KiB) exceeds the LDS, so each transform splits
+// into a column pass over the top 6 index bits (64 residues per thread,
+// column c = low 10 bits) and a block pass over 1024-point blocks, as in the
+// standalone NTT.  Per chunk of polynomials:
+//   1. top_blocks: inverse block stages of limb top, ct_in -> A;
+//   2. cols: inverse column stages of A, N^-1, centring, then for every
+//      lower limb l the forward column stages of r mod q_l -> B[l]
+//      (the centred coefficients stay in registers across the limbs);
+//   3. blocks_combine: forward block stages of B[l], then
+//      (c_l - .) q_top^-1 mod q_l -> ct_out.
+// HBM traffic per polynomial: 2 + 2 (top) + 4 (per lower limb) row transfers
+// instead of the minimum 1 + 2 per lower limb.
+constexpr int kColLogE = 6;
+constexpr int kColThreads = 256;
+constexpr int kBlkLogB = 10;
+constexpr int kBlkLogE = 4;
+constexpr int kBlkThreads = 1 << (kBlkLogB - kBlkLogE);
+constexpr int kBlocksPerRow = 1 << (16 - kBlkLogB);
+constexpr uint32_t kChunkPolys16 = 256;  // polynomials per pass: workspace (1 + top) x 64 MiB
 
-// A[p] = in[p][top]  for p < polys
-__global__ __launch_bounds__(kT) void gather_top_kernel(const uint32_t* __restrict__ in,
-                                                        uint32_t* __restrict__ A, uint32_t limbs,
-                                                        size_t polys) {
-  const size_t words = polys << 16;
-  const size_t stride = static_cast<size_t>(gridDim.x) * kT;
-  for (size_t i = static_cast<size_t>(blockIdx.x) * kT + threadIdx.x; i < words; i += stride) {
-    const size_t p = i >> 16, k = i & 0xFFFF;
-    A[i] = in[((p * limbs) + limbs - 1) * 65536 + k];
-  }
-}
-
-// B = centred(A) mod q_l, A holding residues mod q_top
-__global__ __launch_bounds__(kT) void centre_reduce_kernel(Tables tb, const uint32_t* __restrict__ A,
-                                                           uint32_t* __restrict__ B, uint32_t top,
-                                                           uint32_t l, size_t words) {
-  const uint32_t qt = tb.q[top], q = tb.q[l];
-  const size_t stride = static_cast<size_t>(gridDim.x) * kT;
-  for (size_t i = static_cast<size_t>(blockIdx.x) * kT + threadIdx.x; i < words; i += stride) {
-    const uint32_t x = A[i];
-    const int32_t r = x > (qt >> 1) ? static_cast<int32_t>(x) - static_cast<int32_t>(qt) : static_cast<int32_t>(x);
-    B[i] = static_cast<uint32_t>(r < 0 ? r + static_cast<int32_t>(q) : r);
-  }
-}
-
-// out[p][l] = (in[p][l] - B[p]) * q_top^-1 mod q_l
-__global__ __launch_bounds__(kT) void combine_kernel(Tables tb, const uint32_t* __restrict__ in,
-                                                     const uint32_t* __restrict__ B,
-                                                     uint32_t* __restrict__ out, uint32_t limbs,
-                                                     uint32_t l, size_t polys) {
+__global__ __launch_bounds__(kBlkThreads) void rescale16_top_blocks_kernel(Tables tb, const uint32_t* __restrict__ in,
+                                                                          uint32_t* __restrict__ A, uint32_t limbs,
+                                                                          size_t p0) {
+  using P = Plan<kBlkLogB, kBlkLogE>;
+  __shared__ uint32_t lds[P::lds_words];
+  const size_t r = blockIdx.x / kBlocksPerRow;
+  const uint32_t blk = blockIdx.x % kBlocksPerRow;
+  const uint32_t t = threadIdx.x;
   const uint32_t top = limbs - 1;
-  const uint32_t q = tb.q[l], qi = tb.qinv[top * tb.L + l], qis = tb.qinv_shoup[top * tb.L + l];
-  const size_t words = polys << 16;
-  const size_t stride = static_cast<size_t>(gridDim.x) * kT;
-  for (size_t i = static_cast<size_t>(blockIdx.x) * kT + threadIdx.x; i < words; i += stride) {
-    const size_t p = i >> 16, k = i & 0xFFFF;
-    const uint32_t c = in[(p * limbs + l) * 65536 + k];
-    out[(p * (limbs - 1) + l) * 65536 + k] = mul_shoup(sub_mod(c, B[i], q), qi, qis, q);
+  const uint32_t* a = in + ((p0 + r) * limbs + top) * 65536 + (static_cast<size_t>(blk) << kBlkLogB);
+  uint32_t* o = A + (r << 16) + (static_cast<size_t>(blk) << kBlkLogB);
+  const size_t toff = static_cast<size_t>(top) << 16;
+  uint32_t v[P::E];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<P::NG - 1>(t, j)];
+  inv_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.inv + toff, tb.inv_shoup + toff, tb.q[top], lds);
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) o[P::template pos<0>(t, j)] = v[j];
+}
+
+__global__ __launch_bounds__(kColThreads) void rescale16_cols_kernel(Tables tb, const uint32_t* __restrict__ A,
+                                                                    uint32_t* __restrict__ B, uint32_t limbs,
+                                                                    size_t chunk_words) {
+  using P = Plan<16, kColLogE>;
+  constexpr int kColsPerRow = 1 << (16 - kColLogE);
+  const size_t r = blockIdx.x / (kColsPerRow / kColThreads);
+  const uint32_t c = (blockIdx.x % (kColsPerRow / kColThreads)) * kColThreads + threadIdx.x;
+  const uint32_t top = limbs - 1;
+  const uint32_t qt = tb.q[top];
+  const uint32_t* a = A + (r << 16) + c;
+  uint32_t v[P::E];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<0>(0, j)];
+  const size_t ttop = static_cast<size_t>(top) << 16;
+  inv_group<16, 16, kColLogE, 0>(v, c, 0, tb.inv + ttop, tb.inv_shoup + ttop, qt);  // [0, 2q)
+  const uint32_t ni = tb.ninv[top], nis = tb.ninv_shoup[top];
+  int32_t rc[P::E];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    const uint32_t x = mul_shoup(v[j], ni, nis, qt);
+    rc[j] = x > (qt >> 1) ? static_cast<int32_t>(x) - static_cast<int32_t>(qt) : static_cast<int32_t>(x);
+  }
+  for (uint32_t l = 0; l < top; ++l) {
+    const uint32_t q = tb.q[l];
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = static_cast<uint32_t>(rc[j] < 0 ? rc[j] + static_cast<int32_t>(q) : rc[j]);
+    const size_t tl = static_cast<size_t>(l) << 16;
+    fwd_group<16, 16, kColLogE, 0>(v, c, 0, tb.fwd + tl, tb.fwd_shoup + tl, q);  // [0, 4q)
+    uint32_t* o = B + l * chunk_words + (r << 16) + c;
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) o[P::template pos<0>(0, j)] = v[j];
   }
 }
 
-constexpr size_t kChunkPolys16 = 1024;  // polynomials staged per pass for N = 2^16
-
-uint32_t grid_for(size_t words) {
-  size_t g = (words + kT - 1) / kT;
-  return static_cast<uint32_t>(g > 16384 ? 16384 : g);
+__global__ __launch_bounds__(kBlkThreads) void rescale16_blocks_combine_kernel(
+    Tables tb, const uint32_t* __restrict__ in, const uint32_t* __restrict__ B, uint32_t* __restrict__ out,
+    uint32_t limbs, size_t p0, size_t np, size_t chunk_words) {
+  using P = Plan<kBlkLogB, kBlkLogE>;
+  __shared__ uint32_t lds[P::lds_words];
+  const size_t per_limb = np * kBlocksPerRow;
+  const uint32_t l = static_cast<uint32_t>(blockIdx.x / per_limb);
+  const size_t rem = blockIdx.x % per_limb;
+  const size_t r = rem / kBlocksPerRow;
+  const uint32_t blk = static_cast<uint32_t>(rem % kBlocksPerRow);
+  const uint32_t t = threadIdx.x;
+  const uint32_t top = limbs - 1;
+  const uint32_t q = tb.q[l];
+  const size_t boff = static_cast<size_t>(blk) << kBlkLogB;
+  const uint32_t* b = B + l * chunk_words + (r << 16) + boff;
+  uint32_t v[P::E];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) v[j] = b[P::template pos<0>(t, j)];
+  const size_t tl = static_cast<size_t>(l) << 16;
+  fwd_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+  const uint32_t qi = tb.qinv[top * tb.L + l], qis = tb.qinv_shoup[top * tb.L + l];
+  const uint32_t* c = in + ((p0 + r) * limbs + l) * 65536 + boff;
+  uint32_t* o = out + ((p0 + r) * (limbs - 1) + l) * 65536 + boff;
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    const uint32_t x = P::template pos<P::NG - 1>(t, j);
+    o[x] = mul_shoup(sub_mod(c[x], v[j], q), qi, qis, q);
+  }
 }
 
-// Tables restricted to limb l (so a one-limb batch transforms with q_l).
-Tables limb_view(const Tables& t, uint32_t l) {
-  Tables v = t;
-  const size_t off = static_cast<size_t>(l) << t.log_n;
-  v.q += l;
-  v.fwd += off;
-  v.fwd_shoup += off;
-  v.inv += off;
-  v.inv_shoup += off;
-  v.ninv += l;
-  v.ninv_shoup += l;
-  return v;
-}
+size_t chunk16(size_t polys) { return polys < kChunkPolys16 ? polys : kChunkPolys16; }
 
 hipError_t rescale16(const Tables& t, const uint32_t* in, uint32_t* out, uint32_t count,
                      uint32_t limbs, void* workspace, hipStream_t s) {
   const size_t polys_total = static_cast<size_t>(count) * 2;
-  const size_t chunk = polys_total < kChunkPolys16 ? polys_total : kChunkPolys16;
+  const size_t chunk = chunk16(polys_total);
+  const size_t chunk_words = chunk << 16;
   uint32_t* A = static_cast<uint32_t*>(workspace);  // [chunk][2^16]
-  uint32_t* B = A + (chunk << 16);                  // [chunk][2^16]
+  uint32_t* B = A + chunk_words;                    // [limbs - 1][chunk][2^16]
   const uint32_t top = limbs - 1;
   for (size_t p0 = 0; p0 < polys_total; p0 += chunk) {
     const size_t np = polys_total - p0 < chunk ? polys_total - p0 : chunk;
-    const uint32_t* src = in + p0 * limbs * 65536;
-    uint32_t* dst = out + p0 * (limbs - 1) * 65536;
-    gather_top_kernel<<<grid_for(np << 16), kT, 0, s>>>(src, A, limbs, np);
-    hipError_t e = launch_ntt(limb_view(t, top), A, np, 1, true, s);
-    if (e != hipSuccess) return e;
-    for (uint32_t l = 0; l < top; ++l) {
-      centre_reduce_kernel<<<grid_for(np << 16), kT, 0, s>>>(t, A, B, top, l, np << 16);
-      e = launch_ntt(limb_view(t, l), B, np, 1, false, s);
-      if (e != hipSuccess) return e;
-      combine_kernel<<<grid_for(np << 16), kT, 0, s>>>(t, src, B, dst, limbs, l, np);
-    }
+    rescale16_top_blocks_kernel<<<static_cast<uint32_t>(np * kBlocksPerRow), kBlkThreads, 0, s>>>(t, in, A, limbs, p0);
+    rescale16_cols_kernel<<<static_cast<uint32_t>(np * ((1 << (16 - kColLogE)) / kColThreads)), kColThreads, 0, s>>>(
+        t, A, B, limbs, chunk_words);
+    rescale16_blocks_combine_kernel<<<static_cast<uint32_t>(top * np * kBlocksPerRow), kBlkThreads, 0, s>>>(
+        t, in, B, out, limbs, p0, np, chunk_words);
   }
   return hipGetLastError();
 }
@@ -155,11 +192,9 @@ hipError_t launch_rescale_whole(const Tables& t, const uint32_t* in, uint32_t* o
 
 }  // namespace
 
-size_t rescale_workspace_bytes(const Tables& t, uint32_t count) {
+size_t rescale_workspace_bytes(const Tables& t, uint32_t count, uint32_t limbs) {
   if (t.log_n < 16) return 0;
-  const size_t polys = static_cast<size_t>(count) * 2;
-  const size_t chunk = polys < kChunkPolys16 ? polys : kChunkPolys16;
-  return 2 * (chunk << 16) * sizeof(uint32_t);
+  return static_cast<size_t>(limbs) * (chunk16(static_cast<size_t>(count) * 2) << 16) * sizeof(uint32_t);
 }
 
 hipError_t launch_rescale(const Tables& t, const uint32_t* ct_in, uint32_t* ct_out, uint32_t count,
