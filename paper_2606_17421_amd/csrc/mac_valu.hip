@@ -4,8 +4,9 @@
 // thread owns one (component, NTT slot) column and kRows output rows, keeps
 // u64 accumulators fed by v_mad_u64_u32, and reduces every 15 products
 // (15 * 2^60 + 2^30 < 2^64).  Weights are wave-uniform (scalar loads).
-// Full-polynomial weights: slot-wise products streamed once from HBM; each
-// thread owns one (output, limb, slot) and both ciphertext components.
+// Full-polynomial weights: slot-wise products, the plaintexts streamed once
+// from HBM; each thread owns one (limb, slot), both ciphertext components and
+// a group of output rows.
 #include "ckks_internal.hpp"
 
 namespace ckks {
@@ -56,36 +57,77 @@ __global__ __launch_bounds__(kThreads) void mac_scalar_valu_kernel(
   }
 }
 
+// Full-polynomial weights: thread = (limb l, slots k .. k+3) for kPolyRows
+// outputs j0 .. j0 + kPolyRows - 1, with 16-byte loads.  Each ciphertext
+// residue quad is loaded once per kPolyRows outputs; every plaintext residue
+// is read exactly once.  Workgroups with the same (l, slot block) and
+// consecutive row groups are adjacent in launch order, so the shared
+// ciphertext columns are served from L2.
+constexpr int kPolyRows = 4;
+constexpr int kPolySlots = 4;
+
 __global__ __launch_bounds__(kThreads) void mac_poly_kernel(
     Tables tb, const uint32_t* __restrict__ pt, const uint32_t* __restrict__ ct_in,
-    uint32_t* __restrict__ ct_out, uint32_t d_in, uint32_t limbs) {
+    uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
   const uint32_t n = tb.n;
-  const uint32_t blocks_per_row = n / kThreads;
-  // blockIdx.x = (j * limbs + l) * blocks_per_row + kb
-  const size_t jl = blockIdx.x / blocks_per_row;
-  const uint32_t k = (blockIdx.x % blocks_per_row) * kThreads + threadIdx.x;
-  const uint32_t l = static_cast<uint32_t>(jl % limbs);
-  const size_t j = jl / limbs;
+  const uint32_t groups = (d_out + kPolyRows - 1) / kPolyRows;
+  const uint32_t blocks_per_row = n / (kThreads * kPolySlots);
+  // blockIdx.x = (l * blocks_per_row + kb) * groups + g
+  const uint32_t g = blockIdx.x % groups;
+  const uint32_t lk = blockIdx.x / groups;
+  const uint32_t l = lk / blocks_per_row;
+  const uint32_t k = ((lk % blocks_per_row) * kThreads + threadIdx.x) * kPolySlots;
+  const uint32_t j0 = g * kPolyRows;
+  const uint32_t rows = d_out - j0 < kPolyRows ? d_out - j0 : kPolyRows;  // workgroup-uniform
   const uint32_t q = tb.q[l];
   const double qr = tb.q_recip[l];
   const size_t ln = static_cast<size_t>(limbs) * n;
-  const uint32_t* p_ptr = pt + (j * d_in * limbs + l) * n + k;
-  const uint32_t* x_ptr = ct_in + static_cast<size_t>(l) * n + k;
-  uint64_t a0 = 0, a1 = 0;
+  const uint4* p_ptr = reinterpret_cast<const uint4*>(pt + (static_cast<size_t>(j0) * d_in * limbs + l) * n + k);
+  const size_t p_row = static_cast<size_t>(d_in) * ln / 4;  // one output's plaintexts, in uint4
+  const size_t ln4 = ln / 4;
+  const uint4* x_ptr = reinterpret_cast<const uint4*>(ct_in + static_cast<size_t>(l) * n + k);
+  uint64_t a0[kPolyRows][kPolySlots], a1[kPolyRows][kPolySlots];
+#pragma unroll
+  for (int r = 0; r < kPolyRows; ++r)
+#pragma unroll
+    for (int e = 0; e < kPolySlots; ++e) a0[r][e] = a1[r][e] = 0;
   uint32_t i = 0;
   while (i < d_in) {
     const uint32_t stop = min(d_in, i + kLazy);
     for (; i < stop; ++i) {
-      const uint64_t p = p_ptr[i * ln];
-      a0 += p * x_ptr[(2ull * i) * ln];
-      a1 += p * x_ptr[(2ull * i + 1) * ln];
+      const uint4 x0 = x_ptr[(2ull * i) * ln4], x1 = x_ptr[(2ull * i + 1) * ln4];
+      const uint32_t xs0[4] = {x0.x, x0.y, x0.z, x0.w}, xs1[4] = {x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int r = 0; r < kPolyRows; ++r) {
+        if (r < rows) {
+          const uint4 pv = p_ptr[r * p_row + static_cast<size_t>(i) * ln4];
+          const uint32_t ps[4] = {pv.x, pv.y, pv.z, pv.w};
+#pragma unroll
+          for (int e = 0; e < kPolySlots; ++e) {
+            a0[r][e] += static_cast<uint64_t>(ps[e]) * xs0[e];
+            a1[r][e] += static_cast<uint64_t>(ps[e]) * xs1[e];
+          }
+        }
+      }
     }
-    a0 = reduce_u64(a0, q, qr);
-    a1 = reduce_u64(a1, q, qr);
+#pragma unroll
+    for (int r = 0; r < kPolyRows; ++r)
+#pragma unroll
+      for (int e = 0; e < kPolySlots; ++e) {
+        a0[r][e] = reduce_u64(a0[r][e], q, qr);
+        a1[r][e] = reduce_u64(a1[r][e], q, qr);
+      }
   }
-  uint32_t* o = ct_out + (j * 2 * limbs + l) * n + k;
-  o[0] = static_cast<uint32_t>(a0);
-  o[ln] = static_cast<uint32_t>(a1);
+#pragma unroll
+  for (int r = 0; r < kPolyRows; ++r) {
+    if (r < rows) {
+      uint4* o = reinterpret_cast<uint4*>(ct_out + ((static_cast<size_t>(j0 + r) * 2) * limbs + l) * n + k);
+      o[0] = make_uint4(static_cast<uint32_t>(a0[r][0]), static_cast<uint32_t>(a0[r][1]),
+                        static_cast<uint32_t>(a0[r][2]), static_cast<uint32_t>(a0[r][3]));
+      o[ln4] = make_uint4(static_cast<uint32_t>(a1[r][0]), static_cast<uint32_t>(a1[r][1]),
+                          static_cast<uint32_t>(a1[r][2]), static_cast<uint32_t>(a1[r][3]));
+    }
+  }
 }
 
 __global__ __launch_bounds__(kThreads) void zero_kernel(uint32_t* p, size_t words) {
@@ -107,8 +149,8 @@ hipError_t launch_mac_scalar_valu(const Tables& t, const uint32_t* w_enc, const 
 hipError_t launch_mac_poly(const Tables& t, const uint32_t* pt, const uint32_t* ct_in,
                            uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
                            hipStream_t s) {
-  const size_t grid = static_cast<size_t>(d_out) * limbs * (t.n / kThreads);
-  mac_poly_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, s>>>(t, pt, ct_in, ct_out, d_in, limbs);
+  const size_t grid = static_cast<size_t>((d_out + kPolyRows - 1) / kPolyRows) * limbs * (t.n / (kThreads * kPolySlots));
+  mac_poly_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, s>>>(t, pt, ct_in, ct_out, d_out, d_in, limbs);
   return hipGetLastError();
 }
 
