@@ -1,0 +1,144 @@
+"""GPU parity at the edges of the kernels' tilings and arithmetic bounds.
+
+* The matrix-core MAC over several row, column and k tiles with ragged tails
+  in every dimension, and at the largest d_in its exact epilogue allows
+  (4096), with operands that make the shift-class sums as large as valid
+  residues can; one past that limit the library refuses the matrix-core path
+  and its automatic choice takes the VALU kernel.
+* Rescale at the largest chain (16 limbs) and, at N = 2^16, over more
+  polynomials than one staging chunk holds (a ragged second chunk).
+* The poly MAC with an output count that is not a multiple of its row group.
+
+Everything is compared with the CPU oracle, bit for bit.
+"""
+import numpy as np
+import pytest
+
+from oracle import linear as OL
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+_CTX = {}
+
+
+def ctx_for(ck, log_n, limbs):
+    key = (log_n, limbs)
+    if key not in _CTX:
+        _CTX[key] = ck.Context(log_n, limbs)
+    return _CTX[key]
+
+
+def residues(seed, prefix, qs, n):
+    return gen.uniform_residues(np.random.default_rng(seed), prefix, qs, n)
+
+
+def run_mac(ck, ctx, w, ct, d_out, d_in, limbs, algo):
+    ck.ckks_ctx_set_mac_algo(ctx, algo)
+    try:
+        ws_bytes = ck.ckks_workspace_bytes(ctx, ck.CKKS_OP_MAC_SCALAR, d_out, d_in, limbs)
+        ws = ck.empty_u32((max(ws_bytes, 16) // 4 + 4,))
+        out = ck.empty_u32((d_out, 2, limbs, ctx.n))
+        ck.ckks_linear_mac_scalar(ctx, ck.to_device(w), ck.to_device(ct), out, d_out, d_in, limbs, ws)
+        return ck.to_host_u32(out)
+    finally:
+        ck.ckks_ctx_set_mac_algo(ctx, ck.CKKS_MAC_AUTO)
+
+
+@pytest.mark.parametrize("algo", ["valu", "mfma"])
+def test_mac_scalar_multitile_ragged(gpu_lib, algo):
+    """300 outputs (3 row tiles, the last 44 rows), 200 inputs (4 k-steps, the
+    last 8 deep), 64 column tiles, 3 limbs; general residues as weights."""
+    ck = gpu_lib
+    log_n, limbs, d_in, d_out = 10, 3, 200, 300
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, n = ctx.moduli, ctx.n
+    rng = np.random.default_rng(4242)
+    w = np.stack([rng.integers(0, q, (d_out, d_in), dtype=np.uint64) for q in qs], -1).astype(np.uint32)
+    ct = residues(4243, (d_in, 2), qs, n)
+    got = run_mac(ck, ctx, w, ct, d_out, d_in, limbs, ck.CKKS_MAC_VALU if algo == "valu" else ck.CKKS_MAC_MFMA)
+    assert np.array_equal(got, OL.mac_scalar(w, ct, qs).astype(np.uint32))
+
+
+@pytest.mark.parametrize("case", ["most_negative", "most_positive", "random"])
+def test_mac_mfma_at_the_exactness_bound(gpu_lib, case):
+    """d_in = 4096, the largest the exact digit-split epilogue allows.  Weights
+    whose centred values are -(q-1)/2 or (q-1)/2 (four large digits) against
+    residues q - 1 drive every shift-class sum to its largest magnitude for
+    valid inputs; random residues cover general digit patterns."""
+    ck = gpu_lib
+    log_n, limbs, d_in, d_out = 10, 2, 4096, 16
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, n = ctx.moduli, ctx.n
+    if case == "random":
+        rng = np.random.default_rng(77)
+        w = np.stack([rng.integers(0, q, (d_out, d_in), dtype=np.uint64) for q in qs], -1).astype(np.uint32)
+        ct = residues(78, (d_in, 2), qs, n)
+    else:
+        wv = [(q + 1) // 2 if case == "most_negative" else (q - 1) // 2 for q in qs]
+        w = np.empty((d_out, d_in, limbs), dtype=np.uint32)
+        w[:] = np.array(wv, dtype=np.uint32)
+        ct = np.empty((d_in, 2, limbs, n), dtype=np.uint32)
+        ct[:] = (np.array(qs, dtype=np.uint32) - 1)[:, None]
+    got = run_mac(ck, ctx, w, ct, d_out, d_in, limbs, ck.CKKS_MAC_MFMA)
+    assert np.array_equal(got, OL.mac_scalar(w, ct, qs).astype(np.uint32))
+
+
+def test_mac_above_the_matrix_core_limit(gpu_lib):
+    """d_in = 4097: the matrix-core path is refused; the automatic choice runs
+    the VALU kernel and is exact."""
+    ck = gpu_lib
+    log_n, limbs, d_in, d_out = 10, 1, 4097, 2
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, n = ctx.moduli, ctx.n
+    rng = np.random.default_rng(99)
+    w = rng.integers(0, qs[0], (d_out, d_in, 1), dtype=np.uint64).astype(np.uint32)
+    ct = residues(100, (d_in, 2), qs[:1], n)
+    with pytest.raises(ck.CkksError) as e:
+        run_mac(ck, ctx, w, ct, d_out, d_in, limbs, ck.CKKS_MAC_MFMA)
+    assert e.value.code == ck.CKKS_E_UNSUPPORTED
+    assert ck.ckks_workspace_bytes(ctx, ck.CKKS_OP_MAC_SCALAR, d_out, d_in, limbs) == 0
+    got = run_mac(ck, ctx, w, ct, d_out, d_in, limbs, ck.CKKS_MAC_AUTO)
+    assert np.array_equal(got, OL.mac_scalar(w, ct, qs[:1]).astype(np.uint32))
+
+
+def test_rescale_longest_chain(gpu_lib):
+    ck = gpu_lib
+    log_n, limbs, count = 10, 16, 2
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, psis, n = ctx.moduli, ctx.roots, ctx.n
+    ct = residues(1616, (count, 2), qs, n)
+    out = ck.empty_u32((count, 2, limbs - 1, n))
+    ck.ckks_rescale(ctx, ck.to_device(ct), out, count, limbs)
+    assert np.array_equal(ck.to_host_u32(out), OL.rescale(ct, qs, psis, log_n).astype(np.uint32))
+
+
+def test_rescale_n16_across_staging_chunks(gpu_lib):
+    """130 ciphertexts = 260 polynomials at N = 2^16: one full staging chunk of
+    256 and a ragged one of 4; sampled ciphertexts from both are checked."""
+    ck = gpu_lib
+    log_n, limbs, count = 16, 3, 130
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, psis, n = ctx.moduli, ctx.roots, ctx.n
+    ct = residues(6516, (count, 2), qs, n)
+    ws_bytes = ck.ckks_workspace_bytes(ctx, ck.CKKS_OP_RESCALE, count, 0, limbs)
+    ws = ck.empty_u32((ws_bytes // 4,))
+    out = ck.empty_u32((count, 2, limbs - 1, n))
+    ck.ckks_rescale(ctx, ck.to_device(ct), out, count, limbs, ws)
+    got = ck.to_host_u32(out)
+    for b in (0, 127, 128, 129):
+        want = OL.rescale(ct[b:b + 1], qs, psis, log_n)[0].astype(np.uint32)
+        assert np.array_equal(got[b], want), f"ciphertext {b}"
+
+
+def test_mac_poly_ragged_row_group(gpu_lib):
+    """7 outputs: one full group of four rows and a ragged group of three."""
+    ck = gpu_lib
+    log_n, limbs, d_in, d_out = 11, 2, 6, 7
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, n = ctx.moduli, ctx.n
+    pt = residues(71, (d_out, d_in), qs, n)
+    ct = residues(72, (d_in, 2), qs, n)
+    out = ck.empty_u32((d_out, 2, limbs, n))
+    ck.ckks_linear_mac_poly(ctx, ck.to_device(pt), ck.to_device(ct), out, d_out, d_in, limbs)
+    assert np.array_equal(ck.to_host_u32(out), OL.mac_poly(pt, ct, qs).astype(np.uint32))
