@@ -452,10 +452,8 @@ int ckks_linear_encode_poly(const ckks_ctx* ctx, const double* slots, uint32_t c
   if (int rc = check_ptr(pt, "pt")) return rc;
   DeviceGuard guard(ctx->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = ckks::launch_encode_poly_coeffs(ctx->t, slots, count, limbs, scale, pt, s);
-  if (e != hipSuccess) return hip_fail(e, "encode_poly launch");
-  e = ckks::launch_ntt(ctx->t, pt, static_cast<size_t>(count) * limbs, limbs, false, s);
-  return e == hipSuccess ? ok() : hip_fail(e, "encode_poly ntt launch");
+  hipError_t e = ckks::launch_encode_poly(ctx->t, slots, count, limbs, scale, pt, s);
+  return e == hipSuccess ? ok() : hip_fail(e, "encode_poly launch");
 }
 
 static int check_mac_shapes(const ckks_ctx* ctx, uint32_t d_out, uint32_t d_in) {

@@ -103,9 +103,9 @@ hipError_t launch_ntt(const Tables& t, uint32_t* rows, size_t count_rows, uint32
 hipError_t launch_encode_scalar(const Tables& t, const double* w, size_t count, uint32_t limbs,
                                 double scale, uint32_t* w_enc, hipStream_t s);
 
-// Coefficient-form residues pt[count][limbs][N] of the encoded slot vectors.
-hipError_t launch_encode_poly_coeffs(const Tables& t, const double* slots, uint32_t count,
-                                     uint32_t limbs, double scale, uint32_t* pt, hipStream_t s);
+// NTT-form residues pt[count][limbs][N] of the encoded slot vectors (log_n <= 15).
+hipError_t launch_encode_poly(const Tables& t, const double* slots, uint32_t count, uint32_t limbs,
+                              double scale, uint32_t* pt, hipStream_t s);
 
 hipError_t launch_mac_scalar_valu(const Tables& t, const uint32_t* w_enc, const uint32_t* ct_in,
                                   uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,

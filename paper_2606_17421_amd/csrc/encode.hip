@@ -9,7 +9,7 @@
 // reordering (v_n = y_2n, v_{M-1-n} = y_{2n+1}; X_k = Re(exp(-i pi k/2M) V_k),
 // V = DFT_M(v)), and the real DFT of length M is folded into one complex DFT
 // of length P = M/2, run in LDS in fp64 (radix-2 decimation in frequency).
-#include "ckks_internal.hpp"
+#include "ntt_core.hpp"
 
 namespace ckks {
 namespace {
@@ -32,28 +32,33 @@ __device__ __forceinline__ double2 cmul(double2 a, double2 b) {
 __device__ __forceinline__ double2 cadd(double2 a, double2 b) { return make_double2(a.x + b.x, a.y + b.y); }
 __device__ __forceinline__ double2 csub(double2 a, double2 b) { return make_double2(a.x - b.x, a.y - b.y); }
 
+// Fused full-polynomial encode: coefficients and the forward NTT of every limb
+// in one workgroup per slot vector, with the whole-polynomial transform's
+// thread count.  The spectral buffer (P double2) and the transform's exchange
+// buffer share the LDS.  When every rounded coefficient fits in int32 (the
+// CKKS-scaled weights of the workloads) each thread keeps its 2P/T of them in
+// registers; per limb it writes the residues of their four mirrored positions
+// into the exchange buffer and the transform starts from there (group-0
+// layout).  Otherwise the workgroup writes every limb's coefficient residues
+// to its output rows first and transforms the rows in place from there.
 template <int LOGN>
-struct EncPlan {
-  static constexpr int N = 1 << LOGN;
-  static constexpr int M = N / 2;
-  static constexpr int LOGP = LOGN - 2;
-  static constexpr int P = N / 4;
-  static constexpr int T = P / 2 < 1024 ? P / 2 : 1024;
+struct FusedPlan {
+  using W = WholePlan<LOGN>;
+  using NP = typename W::P;
+  static constexpr int N = 1 << LOGN, M = N / 2, LOGP = LOGN - 2, P = N / 4;
+  static constexpr int T = NP::T;
+  static constexpr int KPT = P / T;  // spectral outputs k per thread
+  static constexpr int LDS_WORDS = (P * 4 > NP::lds_words) ? P * 4 : NP::lds_words;
 };
 
-// One workgroup per slot vector: writes coefficient-form residues pt[b][l][0..N).
+// Slots -> spectrum -> rounded coefficients p(k), p(k + P) for the thread's k
+// (k = t + T i), as exact doubles.  Ends with every thread done reading LDS.
 template <int LOGN>
-__global__ __launch_bounds__(EncPlan<LOGN>::T) void encode_poly_coeffs_kernel(
-    Tables tb, const double* __restrict__ slots, uint32_t limbs, double scale,
-    uint32_t* __restrict__ pt) {
-  using EP = EncPlan<LOGN>;
-  constexpr int N = EP::N, M = EP::M, P = EP::P, T = EP::T;
-  __shared__ double2 a[P];
-  const size_t b = blockIdx.x;
-  const double* z = slots + b * M;
-  uint32_t* out = pt + b * static_cast<size_t>(limbs) * N;
-
-  // c_n = v_2n + i v_2n+1, v_m = y_{u(m)}, u(m) = 2m (m < M/2) or 2(M-1-m)+1.
+__device__ __forceinline__ bool encode_spectrum(const Tables& tb, const double* __restrict__ z, double scale,
+                                                double2* a, double (&p_lo)[FusedPlan<LOGN>::KPT],
+                                                double (&p_hi)[FusedPlan<LOGN>::KPT]) {
+  using FP = FusedPlan<LOGN>;
+  constexpr int M = FP::M, P = FP::P, T = FP::T, N = FP::N;
   for (int n = threadIdx.x; n < P; n += T) {
     const int m0 = 2 * n, m1 = 2 * n + 1;
     const int u0 = m0 < M / 2 ? 2 * m0 : 2 * (M - 1 - m0) + 1;
@@ -61,52 +66,137 @@ __global__ __launch_bounds__(EncPlan<LOGN>::T) void encode_poly_coeffs_kernel(
     a[n] = make_double2(z[tb.slot_perm[u0]], z[tb.slot_perm[u1]]);
   }
   __syncthreads();
-
-  // Radix-2 DIF DFT of length P (forward sign); output in bit-reversed order.
-  for (int s = 0; s < EP::LOGP; ++s) {
+  for (int s = 0; s < FP::LOGP; ++s) {
     const int d = P >> (s + 1);
     for (int idx = threadIdx.x; idx < P / 2; idx += T) {
       const int i = idx & (d - 1);
-      const int x = ((idx >> (EP::LOGP - 1 - s)) << (EP::LOGP - s)) | i;  // (idx / d) * 2d + i
+      const int x = ((idx >> (FP::LOGP - 1 - s)) << (FP::LOGP - s)) | i;
       const double2 U = a[x], V = a[x + d];
       a[x] = cadd(U, V);
       a[x + d] = cmul(csub(U, V), tb.fft_tw[i << s]);
     }
     __syncthreads();
   }
-
   const double two_over_n = 2.0 / N;
-  for (int k = threadIdx.x; k < P; k += T) {
-    const int kr = static_cast<int>(__brev(static_cast<uint32_t>(k)) >> (32 - EP::LOGP));
+  bool fits = true;
+#pragma unroll
+  for (int i = 0; i < FP::KPT; ++i) {
+    const int k = threadIdx.x + T * i;
+    const int kr = static_cast<int>(__brev(static_cast<uint32_t>(k)) >> (32 - FP::LOGP));
     const int km = (P - k) & (P - 1);
-    const int kmr = static_cast<int>(__brev(static_cast<uint32_t>(km)) >> (32 - EP::LOGP));
+    const int kmr = static_cast<int>(__brev(static_cast<uint32_t>(km)) >> (32 - FP::LOGP));
     const double2 ck = a[kr];
     const double2 cm = a[kmr];
     const double2 cmc = make_double2(cm.x, -cm.y);
     const double2 e = make_double2(0.5 * (ck.x + cmc.x), 0.5 * (ck.y + cmc.y));
-    const double2 dd = csub(ck, cmc);                      // O = dd / (2i) = (dd.y, -dd.x) / 2
+    const double2 dd = csub(ck, cmc);
     const double2 o = make_double2(0.5 * dd.y, -0.5 * dd.x);
     const double2 wo = cmul(tb.rfft_tw[k], o);
-    const double2 v_lo = cadd(e, wo);                      // V_k
-    const double2 v_hi = csub(e, wo);                      // V_{k+P}
+    const double2 v_lo = cadd(e, wo);
+    const double2 v_hi = csub(e, wo);
     const double2 t_lo = tb.dct_tw[k], t_hi = tb.dct_tw[k + P];
-    const double x_lo = t_lo.x * v_lo.x - t_lo.y * v_lo.y;  // Re(exp(-i pi k/2M) V_k)
-    const double x_hi = t_hi.x * v_hi.x - t_hi.y * v_hi.y;
-    const double p_lo = rint(scale * (two_over_n * x_lo));
-    const double p_hi = rint(scale * (two_over_n * x_hi));
-    const int k_hi = k + P;
+    p_lo[i] = rint(scale * (two_over_n * (t_lo.x * v_lo.x - t_lo.y * v_lo.y)));
+    p_hi[i] = rint(scale * (two_over_n * (t_hi.x * v_hi.x - t_hi.y * v_hi.y)));
+    fits = fits && fabs(p_lo[i]) < 2147483648.0 && fabs(p_hi[i]) < 2147483648.0;
+  }
+  return __syncthreads_and(fits);
+}
+
+// Residues mod q of coefficients k, k + P and their mirrors at index x of
+// `row` through `at` (m_{N-k} = -m_k for 0 < k < M; m_{N/2} = 0).
+template <int LOGN, typename At>
+__device__ __forceinline__ void scatter_residues(At at, int k, double p_lo, double p_hi, uint32_t q, double qr) {
+  using FP = FusedPlan<LOGN>;
+  constexpr int N = FP::N, M = FP::M, P = FP::P;
+  const uint32_t r_lo = reduce_f64_int(p_lo, q, qr);
+  const uint32_t r_hi = reduce_f64_int(p_hi, q, qr);
+  at(k) = r_lo;
+  at(k + P) = r_hi;
+  if (k == 0) at(M) = 0;
+  else at(N - k) = r_lo ? q - r_lo : 0;
+  at(N - k - P) = r_hi ? q - r_hi : 0;
+}
+
+template <int LOGN>
+__global__ __launch_bounds__(FusedPlan<LOGN>::T, WholePlan<LOGN>::kWavesPerSimd) void encode_poly_ntt_kernel(
+    Tables tb, const double* __restrict__ slots, uint32_t limbs, double scale, uint32_t* __restrict__ pt) {
+  using FP = FusedPlan<LOGN>;
+  using NP = typename FP::NP;
+  constexpr int LOGE = FP::W::LOGE;
+  constexpr int N = FP::N, T = FP::T;
+  __shared__ __align__(16) uint32_t lds[FP::LDS_WORDS];
+  const size_t b = blockIdx.x;
+  const double* z = slots + b * FP::M;
+  uint32_t* out = pt + b * static_cast<size_t>(limbs) * N;
+  const uint32_t t = threadIdx.x;
+
+  double p_lo[FP::KPT], p_hi[FP::KPT];
+  const bool all_fit = encode_spectrum<LOGN>(tb, z, scale, reinterpret_cast<double2*>(lds), p_lo, p_hi);
+  if (all_fit) {  // workgroup-uniform
+    int32_t c_lo[FP::KPT], c_hi[FP::KPT];
+#pragma unroll
+    for (int i = 0; i < FP::KPT; ++i) {
+      c_lo[i] = static_cast<int32_t>(p_lo[i]);
+      c_hi[i] = static_cast<int32_t>(p_hi[i]);
+    }
+    // Natural (unpadded) order for the scatter: lane t touches index t + const
+    // or N - t - const, distinct banks either way.  Index N - k for k = 0 is
+    // index N, a spare word past the row; index N/2 is written 0 separately.
+    uint32_t* b0 = lds + t;                                   // k = t + T i
+    uint32_t* b1 = lds + t + FP::P;                           // k + P
+    uint32_t* b2 = lds + (N - t) - T * (FP::KPT - 1);         // N - k      at offset T (KPT-1-i)
+    uint32_t* b3 = lds + (N - FP::P - t) - T * (FP::KPT - 1); // N - k - P  at offset T (KPT-1-i)
+    for (uint32_t l = 0; l < limbs; ++l) {
+      const uint32_t q = tb.q[l];
+      // x mod q for x < 2^32 by a Shoup product with w = 1: ws = floor(2^32 / q)
+      uint32_t ws = static_cast<uint32_t>(4294967296.0 * tb.q_recip[l]);
+      if (static_cast<uint64_t>(ws) * q > 0xFFFFFFFFull) --ws;
+      if (static_cast<uint64_t>(ws + 1) * q <= 0xFFFFFFFFull) ++ws;
+      uint32_t b31 = 0x80000000u - 2 * q;  // 2^31 mod q (2 q < 2^31 < 4 q)
+      b31 = min(b31, b31 - q);
+      auto residue = [&](int32_t c) {  // c mod q for |c| < 2^31
+        return sub_mod(mul_shoup(static_cast<uint32_t>(c) + 0x80000000u, 1u, ws, q), b31, q);
+      };
+      if (l > 0) __syncthreads();  // the previous transform is done with the LDS
+#pragma unroll
+      for (int i = 0; i < FP::KPT; ++i) {
+        const uint32_t r_lo = residue(c_lo[i]), r_hi = residue(c_hi[i]);
+        b0[T * i] = r_lo;
+        b1[T * i] = r_hi;
+        b2[T * (FP::KPT - 1 - i)] = r_lo ? q - r_lo : 0;
+        b3[T * (FP::KPT - 1 - i)] = r_hi ? q - r_hi : 0;
+      }
+      if (t == 0) lds[FP::M] = 0;  // m_{N/2} = 0
+      __syncthreads();
+      uint32_t v[NP::E];
+#pragma unroll
+      for (int j = 0; j < NP::E; ++j) v[j] = lds[NP::template pos<0>(t, j)];
+      const size_t tl = static_cast<size_t>(l) << LOGN;
+      fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+      uint32_t* row = out + static_cast<size_t>(l) * N;
+#pragma unroll
+      for (int j = 0; j < NP::E; ++j) row[NP::template pos<NP::NG - 1>(t, j)] = v[j];
+    }
+  } else {
     for (uint32_t l = 0; l < limbs; ++l) {
       const uint32_t q = tb.q[l];
       const double qr = tb.q_recip[l];
       uint32_t* row = out + static_cast<size_t>(l) * N;
-      const uint32_t r_lo = reduce_f64_int(p_lo, q, qr);
-      const uint32_t r_hi = reduce_f64_int(p_hi, q, qr);
-      row[k] = r_lo;
-      row[k_hi] = r_hi;
-      // m_{N-k} = -m_k for 0 < k < M; m_{N/2} = 0.
-      if (k == 0) row[M] = 0;
-      else row[N - k] = r_lo ? q - r_lo : 0;
-      row[N - k_hi] = r_hi ? q - r_hi : 0;
+#pragma unroll
+      for (int i = 0; i < FP::KPT; ++i)
+        scatter_residues<LOGN>([&](int x) -> uint32_t& { return row[x]; }, static_cast<int>(t) + T * i, p_lo[i],
+                               p_hi[i], q, qr);
+    }
+    for (uint32_t l = 0; l < limbs; ++l) {
+      __syncthreads();  // coefficient rows written; the previous transform is done with the LDS
+      uint32_t* row = out + static_cast<size_t>(l) * N;
+      uint32_t v[NP::E];
+#pragma unroll
+      for (int j = 0; j < NP::E; ++j) v[j] = row[NP::template pos<0>(t, j)];
+      const size_t tl = static_cast<size_t>(l) << LOGN;
+      fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, tb.q[l], lds);
+#pragma unroll
+      for (int j = 0; j < NP::E; ++j) row[NP::template pos<NP::NG - 1>(t, j)] = v[j];
     }
   }
 }
@@ -114,7 +204,7 @@ __global__ __launch_bounds__(EncPlan<LOGN>::T) void encode_poly_coeffs_kernel(
 template <int LOGN>
 hipError_t launch_poly(const Tables& t, const double* slots, uint32_t count, uint32_t limbs,
                        double scale, uint32_t* pt, hipStream_t s) {
-  encode_poly_coeffs_kernel<LOGN><<<count, EncPlan<LOGN>::T, 0, s>>>(t, slots, limbs, scale, pt);
+  encode_poly_ntt_kernel<LOGN><<<count, FusedPlan<LOGN>::T, 0, s>>>(t, slots, limbs, scale, pt);
   return hipGetLastError();
 }
 
@@ -129,8 +219,8 @@ hipError_t launch_encode_scalar(const Tables& t, const double* w, size_t count, 
   return hipGetLastError();
 }
 
-hipError_t launch_encode_poly_coeffs(const Tables& t, const double* slots, uint32_t count,
-                                     uint32_t limbs, double scale, uint32_t* pt, hipStream_t s) {
+hipError_t launch_encode_poly(const Tables& t, const double* slots, uint32_t count, uint32_t limbs,
+                              double scale, uint32_t* pt, hipStream_t s) {
   if (count == 0) return hipSuccess;
   switch (t.log_n) {
     case 10: return launch_poly<10>(t, slots, count, limbs, scale, pt, s);

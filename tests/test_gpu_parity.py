@@ -220,6 +220,30 @@ def test_encode_poly_within_tolerance(gpu_lib, log_n, limbs, count):
     assert mismatches <= max(2, count * n // 100000)
 
 
+@pytest.mark.parametrize("log_n,limbs", [(10, 3), (15, 2)])
+def test_encode_poly_large_coefficients(gpu_lib, log_n, limbs):
+    """Slots offset by 4.0 at scale 2^30: coefficients beyond 2^31 take the
+    encoder's wide path (every limb's coefficient residues written first, then
+    transformed in place); bit-exact against the oracle's NTT-form residues
+    except at fp64 rounding ties, held to the same decoded-slot bound."""
+    ck = gpu_lib
+    ctx = ctx_for(ck, log_n, max(limbs, 3))
+    qs, psis, n = ctx.moduli[:limbs], ctx.roots[:limbs], 1 << log_n
+    delta = 2.0 ** 30
+    z = 4.0 + gen.poly_weights(np.random.default_rng(log_n + 5), 1, 2, n // 2)[0]
+    pt = ck.empty_u32((2, limbs, n))
+    ck.ckks_linear_encode_poly(ctx, ck.to_device(z), 2, limbs, delta, pt)
+    got = ck.to_host_u32(pt)
+    want = OE.encode_poly(z, delta, qs, psis, log_n).astype(np.uint32)
+    assert np.max(np.abs(OE.round_coeffs(OE.encode_coeffs(z, log_n), delta))) >= 2 ** 31
+    sl_got = _decode_rows(got, qs, psis, log_n, delta)
+    sl_want = _decode_rows(want, qs, psis, log_n, delta)
+    err = np.max(np.abs(sl_got - sl_want))
+    assert err <= 2.0 ** -20 * max(1.0, np.max(np.abs(sl_want))), err
+    rows_equal = int(sum(np.array_equal(got[b, l], want[b, l]) for b in range(2) for l in range(limbs)))
+    print(f"encode_poly large N=2^{log_n}: {rows_equal} of {2 * limbs} limb rows identical")
+
+
 def test_config1_end_to_end(gpu_lib):
     """Tiny encrypted layer: GPU encode + MAC + rescale bit-exact, then decrypts to W.x."""
     ck = gpu_lib
