@@ -57,8 +57,10 @@ __device__ __forceinline__ void fwd_group(uint32_t (&v)[1 << LOGE], uint32_t t, 
   for (int b = P::hi(G); b >= P::lo(G); --b) {
     const int s = LOGN - 1 - b;
     const int lb = b - w;
+    // In group 0 a thread id below 2^w has t >> w = 0: the twiddles are then
+    // workgroup-uniform (scalar loads).
     const uint32_t base = (1u << s) + (blk << (LOGB - 1 - b)) +
-                          ((t >> w) << (w + LOGE - b - 1));
+                          (w >= P::LOGT ? 0u : ((t >> w) << (w + LOGE - b - 1)));
 #pragma unroll
     for (int u = 0; u < (P::E >> (lb + 1)); ++u) {
       const uint32_t idx = base + u;
@@ -89,8 +91,10 @@ __device__ __forceinline__ void inv_group(uint32_t (&v)[1 << LOGE], uint32_t t, 
   for (int b = P::lo(G); b <= P::hi(G); ++b) {
     const int s = LOGN - 1 - b;
     const int lb = b - w;
+    // In group 0 a thread id below 2^w has t >> w = 0: the twiddles are then
+    // workgroup-uniform (scalar loads).
     const uint32_t base = (1u << s) + (blk << (LOGB - 1 - b)) +
-                          ((t >> w) << (w + LOGE - b - 1));
+                          (w >= P::LOGT ? 0u : ((t >> w) << (w + LOGE - b - 1)));
 #pragma unroll
     for (int u = 0; u < (P::E >> (lb + 1)); ++u) {
       const uint32_t idx = base + u;

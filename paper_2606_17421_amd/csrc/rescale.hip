@@ -78,6 +78,26 @@ constexpr int kBlkThreads = 1 << (kBlkLogB - kBlkLogE);
 constexpr int kBlocksPerRow = 1 << (16 - kBlkLogB);
 constexpr uint32_t kChunkPolys16 = 256;  // polynomials per pass: workspace (1 + top) x 64 MiB
 
+
+// A 64-thread block workgroup is one wave, so re-laying its block out between
+// the last group's layout (thread t holds t E .. t E + E - 1) and the
+// coalesced one (thread t holds t + 64 j) needs no barrier: the wave's LDS
+// accesses are in order (wave_barrier keeps the compiler from moving them).
+template <bool TO_LAST>
+__device__ __forceinline__ void block_relayout(uint32_t (&v)[1 << kBlkLogE], uint32_t t, uint32_t* lds) {
+  using P = Plan<kBlkLogB, kBlkLogE>;
+  static_assert(P::T == 64, "one wave per block");
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int j = 0; j < P::E; ++j)
+    lds[lds_pad(TO_LAST ? t + 64 * j : P::template pos<P::NG - 1>(t, j))] = v[j];
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int j = 0; j < P::E; ++j)
+    v[j] = lds[lds_pad(TO_LAST ? P::template pos<P::NG - 1>(t, j) : t + 64 * j)];
+  __builtin_amdgcn_wave_barrier();
+}
+
 __global__ __launch_bounds__(kBlkThreads) void rescale16_top_blocks_kernel(Tables tb, const uint32_t* __restrict__ in,
                                                                           uint32_t* __restrict__ A, uint32_t limbs,
                                                                           size_t p0) {
@@ -92,7 +112,8 @@ __global__ __launch_bounds__(kBlkThreads) void rescale16_top_blocks_kernel(Table
   const size_t toff = static_cast<size_t>(top) << 16;
   uint32_t v[P::E];
 #pragma unroll
-  for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<P::NG - 1>(t, j)];
+  for (int j = 0; j < P::E; ++j) v[j] = a[t + 64 * j];  // coalesced
+  block_relayout<true>(v, t, lds);
   inv_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.inv + toff, tb.inv_shoup + toff, tb.q[top], lds);
 #pragma unroll
   for (int j = 0; j < P::E; ++j) o[P::template pos<0>(t, j)] = v[j];
@@ -155,9 +176,10 @@ __global__ __launch_bounds__(kBlkThreads) void rescale16_blocks_combine_kernel(
   const uint32_t qi = tb.qinv[top * tb.L + l], qis = tb.qinv_shoup[top * tb.L + l];
   const uint32_t* c = in + ((p0 + r) * limbs + l) * 65536 + boff;
   uint32_t* o = out + ((p0 + r) * (limbs - 1) + l) * 65536 + boff;
+  block_relayout<false>(v, t, lds);
 #pragma unroll
   for (int j = 0; j < P::E; ++j) {
-    const uint32_t x = P::template pos<P::NG - 1>(t, j);
+    const uint32_t x = t + 64 * j;  // coalesced
     o[x] = mul_shoup(sub_mod(c[x], v[j], q), qi, qis, q);
   }
 }
