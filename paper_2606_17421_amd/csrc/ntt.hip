@@ -28,11 +28,15 @@ __global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSi
 #pragma unroll
     for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<0>(t, j)];
     fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + toff, tb.fwd_shoup + toff, q, lds);
+    wave_relayout<LOGN, LOGE, false>(v, t, lds);
+    uint32_t* ac = a + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) a[P::template pos<P::NG - 1>(t, j)] = v[j];
+    for (int j = 0; j < P::E; ++j) ac[j << 6] = v[j];
   } else {
+    const uint32_t* ac = a + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<P::NG - 1>(t, j)];
+    for (int j = 0; j < P::E; ++j) v[j] = ac[j << 6];
+    wave_relayout<LOGN, LOGE, true>(v, t, lds);
     inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + toff, tb.inv_shoup + toff, q, lds);
     const uint32_t ni = tb.ninv[l], nis = tb.ninv_shoup[l];
 #pragma unroll
@@ -93,11 +97,13 @@ __global__ __launch_bounds__(1 << (kBlkLogB - kBlkLogE)) void ntt16_blocks_kerne
 #pragma unroll
     for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<0>(t, j)];
     fwd_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.fwd + toff, tb.fwd_shoup + toff, q, lds);
+    wave_relayout<kBlkLogB, kBlkLogE, false>(v, t, lds);
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) a[P::template pos<P::NG - 1>(t, j)] = v[j];
+    for (int j = 0; j < P::E; ++j) a[t + 64 * j] = v[j];  // coalesced (one wave per block)
   } else {
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) v[j] = a[P::template pos<P::NG - 1>(t, j)];
+    for (int j = 0; j < P::E; ++j) v[j] = a[t + 64 * j];
+    wave_relayout<kBlkLogB, kBlkLogE, true>(v, t, lds);
     inv_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.inv + toff, tb.inv_shoup + toff, q, lds);
 #pragma unroll
     for (int j = 0; j < P::E; ++j) a[P::template pos<0>(t, j)] = v[j];

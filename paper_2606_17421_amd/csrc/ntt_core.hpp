@@ -144,6 +144,39 @@ __device__ __forceinline__ void exchange(uint32_t (&v)[1 << LOGE], uint32_t t, u
   for (int j = 0; j < P::E; ++j) v[j] = rb[lds_pad(P::template pos<GT>(0, j))];
 }
 
+// Wave-coalesced layout: element j of lane i of wave a is index
+// a 2^(LOGE+6) + 64 j + i, so a load or store of element j by a wave touches
+// 64 consecutive words.  Each wave holds the same index set in it as in the
+// last group's layout (index t 2^LOGE + j; all indices whose bits from
+// LOGE + 6 up equal a), so the two convert through the wave's own LDS region
+// without a workgroup barrier.  Needs T >= 64 (every plan here).
+template <int LOGE>
+__device__ __forceinline__ uint32_t pos_coalesced(uint32_t t, uint32_t j) {
+  return ((t >> 6) << (LOGE + 6)) + (j << 6) + (t & 63);
+}
+
+template <int LOGB, int LOGE, bool TO_LAST>
+__device__ __forceinline__ void wave_relayout(uint32_t (&v)[1 << LOGE], uint32_t t, uint32_t* lds) {
+  using P = Plan<LOGB, LOGE>;
+  static_assert(P::T >= 64 && P::lo(P::NG - 1) == 0, "whole waves; last group keeps no thread bits low");
+  // t's bits and j's bits of either position are disjoint: base + constant.
+  uint32_t* cb = lds + lds_pad(pos_coalesced<LOGE>(t, 0));
+  uint32_t* lb = lds + lds_pad(P::template pos<P::NG - 1>(t, 0));
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    if constexpr (TO_LAST) cb[lds_pad(j << 6)] = v[j];
+    else lb[lds_pad(P::template pos<P::NG - 1>(0, j))] = v[j];
+  }
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    if constexpr (TO_LAST) v[j] = lb[lds_pad(P::template pos<P::NG - 1>(0, j))];
+    else v[j] = cb[lds_pad(j << 6)];
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
 // Forward transform of one block held in registers in group-0 layout; on
 // return the registers hold group NG-1 layout.
 template <int LOGN, int LOGB, int LOGE, int G = 0>

@@ -29,9 +29,20 @@ __global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSi
   const uint32_t top = limbs - 1;
   const uint32_t qt = tb.q[top];
 
+  // Up to 2^14 the rows are read and written in the wave-coalesced layout
+  // (re-laid out through each wave's LDS region); at 2^15 the extra live
+  // registers of that path cost more than the coalescing gains.
+  constexpr bool kCoalesce = LOGN <= 14;
   uint32_t v[P::E];
+  if constexpr (kCoalesce) {
+    const uint32_t* stop = src + static_cast<size_t>(top) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-  for (int j = 0; j < P::E; ++j) v[j] = src[static_cast<size_t>(top) * N + P::template pos<P::NG - 1>(t, j)];
+    for (int j = 0; j < P::E; ++j) v[j] = stop[j << 6];
+    wave_relayout<LOGN, LOGE, true>(v, t, lds);
+  } else {
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = src[static_cast<size_t>(top) * N + P::template pos<P::NG - 1>(t, j)];
+  }
   const size_t ttop = static_cast<size_t>(top) << LOGN;
   inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + ttop, tb.inv_shoup + ttop, qt, lds);
   const uint32_t ni = tb.ninv[top], nis = tb.ninv_shoup[top];
@@ -49,10 +60,18 @@ __global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSi
     const size_t tl = static_cast<size_t>(l) << LOGN;
     fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
     const uint32_t qi = tb.qinv[top * tb.L + l], qis = tb.qinv_shoup[top * tb.L + l];
+    if constexpr (kCoalesce) {
+      wave_relayout<LOGN, LOGE, false>(v, t, lds);
+      const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
+      uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) {
-      const size_t x = static_cast<size_t>(l) * N + P::template pos<P::NG - 1>(t, j);
-      dst[x] = mul_shoup(sub_mod(src[x], v[j], q), qi, qis, q);
+      for (int j = 0; j < P::E; ++j) dl[j << 6] = mul_shoup(sub_mod(sl[j << 6], v[j], q), qi, qis, q);
+    } else {
+#pragma unroll
+      for (int j = 0; j < P::E; ++j) {
+        const size_t x = static_cast<size_t>(l) * N + P::template pos<P::NG - 1>(t, j);
+        dst[x] = mul_shoup(sub_mod(src[x], v[j], q), qi, qis, q);
+      }
     }
   }
 }
@@ -79,25 +98,6 @@ constexpr int kBlocksPerRow = 1 << (16 - kBlkLogB);
 constexpr uint32_t kChunkPolys16 = 256;  // polynomials per pass: workspace (1 + top) x 64 MiB
 
 
-// A 64-thread block workgroup is one wave, so re-laying its block out between
-// the last group's layout (thread t holds t E .. t E + E - 1) and the
-// coalesced one (thread t holds t + 64 j) needs no barrier: the wave's LDS
-// accesses are in order (wave_barrier keeps the compiler from moving them).
-template <bool TO_LAST>
-__device__ __forceinline__ void block_relayout(uint32_t (&v)[1 << kBlkLogE], uint32_t t, uint32_t* lds) {
-  using P = Plan<kBlkLogB, kBlkLogE>;
-  static_assert(P::T == 64, "one wave per block");
-  __builtin_amdgcn_wave_barrier();
-#pragma unroll
-  for (int j = 0; j < P::E; ++j)
-    lds[lds_pad(TO_LAST ? t + 64 * j : P::template pos<P::NG - 1>(t, j))] = v[j];
-  __builtin_amdgcn_wave_barrier();
-#pragma unroll
-  for (int j = 0; j < P::E; ++j)
-    v[j] = lds[lds_pad(TO_LAST ? P::template pos<P::NG - 1>(t, j) : t + 64 * j)];
-  __builtin_amdgcn_wave_barrier();
-}
-
 __global__ __launch_bounds__(kBlkThreads) void rescale16_top_blocks_kernel(Tables tb, const uint32_t* __restrict__ in,
                                                                           uint32_t* __restrict__ A, uint32_t limbs,
                                                                           size_t p0) {
@@ -113,7 +113,7 @@ __global__ __launch_bounds__(kBlkThreads) void rescale16_top_blocks_kernel(Table
   uint32_t v[P::E];
 #pragma unroll
   for (int j = 0; j < P::E; ++j) v[j] = a[t + 64 * j];  // coalesced
-  block_relayout<true>(v, t, lds);
+  wave_relayout<kBlkLogB, kBlkLogE, true>(v, t, lds);
   inv_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.inv + toff, tb.inv_shoup + toff, tb.q[top], lds);
 #pragma unroll
   for (int j = 0; j < P::E; ++j) o[P::template pos<0>(t, j)] = v[j];
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kBlkThreads) void rescale16_blocks_combine_kernel(
   const uint32_t qi = tb.qinv[top * tb.L + l], qis = tb.qinv_shoup[top * tb.L + l];
   const uint32_t* c = in + ((p0 + r) * limbs + l) * 65536 + boff;
   uint32_t* o = out + ((p0 + r) * (limbs - 1) + l) * 65536 + boff;
-  block_relayout<false>(v, t, lds);
+  wave_relayout<kBlkLogB, kBlkLogE, false>(v, t, lds);
 #pragma unroll
   for (int j = 0; j < P::E; ++j) {
     const uint32_t x = t + 64 * j;  // coalesced
