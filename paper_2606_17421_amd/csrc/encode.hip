@@ -8,7 +8,10 @@
 // with m_{N/2} = 0 and m_{N-k} = -m_k.  X is computed with Makhoul's
 // reordering (v_n = y_2n, v_{M-1-n} = y_{2n+1}; X_k = Re(exp(-i pi k/2M) V_k),
 // V = DFT_M(v)), and the real DFT of length M is folded into one complex DFT
-// of length P = M/2, run in LDS in fp64 (radix-2 decimation in frequency).
+// of length P = M/2, run in LDS in fp64 (decimation in frequency, three
+// radix-2 stages per LDS pass).  The slot vector is staged in LDS with
+// coalesced loads before the Makhoul reordering gathers from it, and the
+// transformed rows leave through the wave-local re-layout as coalesced stores.
 #include "ntt_core.hpp"
 
 namespace ckks {
@@ -31,6 +34,40 @@ __device__ __forceinline__ double2 cmul(double2 a, double2 b) {
 }
 __device__ __forceinline__ double2 cadd(double2 a, double2 b) { return make_double2(a.x + b.x, a.y + b.y); }
 __device__ __forceinline__ double2 csub(double2 a, double2 b) { return make_double2(a.x - b.x, a.y - b.y); }
+
+// R consecutive radix-2 decimation-in-frequency stages s .. s+R-1 of a
+// P = 2^LOGP point complex FFT held in LDS, run in registers: a group is the
+// 2^R elements base + j (P >> (s+R)) that those stages combine with each
+// other; the stage s+r butterfly on (x, x + d), d = P >> (s+r+1), multiplies
+// the difference by tw[(x mod d) << (s+r)].  Same results, in the same
+// positions, as R single stages; one LDS round trip and one barrier.
+template <int LOGP, int R>
+__device__ __forceinline__ void fft_pass(double2* a, int s, const double2* __restrict__ tw, int nthreads) {
+  constexpr int P = 1 << LOGP, G = 1 << R;
+  const int span_lo = P >> (s + R);           // stride between a group's elements
+  for (int g = threadIdx.x; g < (P >> R); g += nthreads) {
+    const int x0 = g & (span_lo - 1);
+    const int base = ((g >> (LOGP - s - R)) << (LOGP - s)) | x0;
+    double2 v[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) v[j] = a[base + j * span_lo];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int h = G >> (r + 1);             // partner distance within the group
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        if (j & h) continue;
+        const int i = x0 + (j & (h - 1)) * span_lo;   // index within the stage's half-block
+        const double2 U = v[j], V = v[j + h];
+        v[j] = cadd(U, V);
+        v[j + h] = cmul(csub(U, V), tw[i << (s + r)]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < G; ++j) a[base + j * span_lo] = v[j];
+  }
+  __syncthreads();
+}
 
 // Fused full-polynomial encode: coefficients and the forward NTT of every limb
 // in one workgroup per slot vector, with the whole-polynomial transform's
@@ -59,24 +96,33 @@ __device__ __forceinline__ bool encode_spectrum(const Tables& tb, const double* 
                                                 double (&p_hi)[FusedPlan<LOGN>::KPT]) {
   using FP = FusedPlan<LOGN>;
   constexpr int M = FP::M, P = FP::P, T = FP::T, N = FP::N;
-  for (int n = threadIdx.x; n < P; n += T) {
-    const int m0 = 2 * n, m1 = 2 * n + 1;
-    const int u0 = m0 < M / 2 ? 2 * m0 : 2 * (M - 1 - m0) + 1;
-    const int u1 = m1 < M / 2 ? 2 * m1 : 2 * (M - 1 - m1) + 1;
-    a[n] = make_double2(z[tb.slot_perm[u0]], z[tb.slot_perm[u1]]);
-  }
-  __syncthreads();
-  for (int s = 0; s < FP::LOGP; ++s) {
-    const int d = P >> (s + 1);
-    for (int idx = threadIdx.x; idx < P / 2; idx += T) {
-      const int i = idx & (d - 1);
-      const int x = ((idx >> (FP::LOGP - 1 - s)) << (FP::LOGP - s)) | i;
-      const double2 U = a[x], V = a[x + d];
-      a[x] = cadd(U, V);
-      a[x + d] = cmul(csub(U, V), tb.fft_tw[i << s]);
+  // Stage the slot vector in LDS with coalesced 16-byte loads, then gather
+  // the Makhoul-ordered pairs from there (the spectrum reuses the same LDS).
+  {
+    double2* zs = a;  // M doubles = P double2
+    const double2* z2 = reinterpret_cast<const double2*>(z);
+#pragma unroll
+    for (int i = 0; i < P / T; ++i) zs[threadIdx.x + T * i] = z2[threadIdx.x + T * i];
+    __syncthreads();
+    const double* zd = reinterpret_cast<const double*>(zs);
+    double2 g[P / T];
+#pragma unroll
+    for (int i = 0; i < P / T; ++i) {
+      const int n = threadIdx.x + T * i;
+      const int m0 = 2 * n, m1 = 2 * n + 1;
+      const int u0 = m0 < M / 2 ? 2 * m0 : 2 * (M - 1 - m0) + 1;
+      const int u1 = m1 < M / 2 ? 2 * m1 : 2 * (M - 1 - m1) + 1;
+      g[i] = make_double2(zd[tb.slot_perm[u0]], zd[tb.slot_perm[u1]]);
     }
     __syncthreads();
+#pragma unroll
+    for (int i = 0; i < P / T; ++i) a[threadIdx.x + T * i] = g[i];
   }
+  __syncthreads();
+  int s = 0;
+  for (; s + 3 <= FP::LOGP; s += 3) fft_pass<FP::LOGP, 3>(a, s, tb.fft_tw, T);
+  if (FP::LOGP - s == 2) fft_pass<FP::LOGP, 2>(a, s, tb.fft_tw, T);
+  if (FP::LOGP - s == 1) fft_pass<FP::LOGP, 1>(a, s, tb.fft_tw, T);
   const double two_over_n = 2.0 / N;
   bool fits = true;
 #pragma unroll
@@ -173,9 +219,10 @@ __global__ __launch_bounds__(FusedPlan<LOGN>::T, WholePlan<LOGN>::kWavesPerSimd)
       for (int j = 0; j < NP::E; ++j) v[j] = lds[NP::template pos<0>(t, j)];
       const size_t tl = static_cast<size_t>(l) << LOGN;
       fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+      wave_relayout<LOGN, LOGE, false>(v, t, lds);  // last-group layout -> wave-coalesced
       uint32_t* row = out + static_cast<size_t>(l) * N;
 #pragma unroll
-      for (int j = 0; j < NP::E; ++j) row[NP::template pos<NP::NG - 1>(t, j)] = v[j];
+      for (int j = 0; j < NP::E; ++j) row[pos_coalesced<LOGE>(t, j)] = v[j];
     }
   } else {
     for (uint32_t l = 0; l < limbs; ++l) {
@@ -195,8 +242,9 @@ __global__ __launch_bounds__(FusedPlan<LOGN>::T, WholePlan<LOGN>::kWavesPerSimd)
       for (int j = 0; j < NP::E; ++j) v[j] = row[NP::template pos<0>(t, j)];
       const size_t tl = static_cast<size_t>(l) << LOGN;
       fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, tb.q[l], lds);
+      wave_relayout<LOGN, LOGE, false>(v, t, lds);
 #pragma unroll
-      for (int j = 0; j < NP::E; ++j) row[NP::template pos<NP::NG - 1>(t, j)] = v[j];
+      for (int j = 0; j < NP::E; ++j) row[pos_coalesced<LOGE>(t, j)] = v[j];
     }
   }
 }
