@@ -18,9 +18,16 @@ inputs (they come from the seeded generators, never from here).
 Decryption is m + e' = INTT(c0 + c1 (.) NTT(s)), lifted by CRT to centred
 integers.
 
+Decrypt-then-encrypt refresh (the DtE equation of section 3.2, ct' =
+Enc(Dec(ct))): the plaintext polynomial m + e' of a ciphertext at any level is
+recovered exactly from its first two limbs by CRT to centred integers (valid
+while |m + e'| < q_0 q_1 / 2), then encrypted afresh, with new randomness,
+under a chosen number of limbs (reading: the refresh acts on the integer
+plaintext polynomial; decoding to slots and re-encoding would round it again).
+
 Parity: pinned (tests/test_oracle_rlwe.py) against the coefficient-domain
-definition -a*s + m + e with the schoolbook product at small N, and by
-round trips.
+definition -a*s + m + e with the schoolbook product at small N, by round
+trips, and (refresh) against a direct fresh encryption of the known m + e.
 """
 from __future__ import annotations
 
@@ -82,3 +89,22 @@ def decrypt(ct, s, qs, psis, log_n: int) -> list[int]:
     for q in qs[:L]:
         Q *= q
     return [centre(c, Q) for c in crt_lift(res, qs[:L])]
+
+
+def refresh(ct, s, a_ntt, e, qs, psis, log_n: int, limbs_out: int) -> np.ndarray:
+    """Decrypt-then-encrypt (section 3.2): ct (B, 2, L_in, N) in NTT form, L_in >= 2.
+
+    Decrypts with limbs 0 and 1 (CRT over q_0 q_1, centred), then returns
+    encrypt(m + e', s, a_ntt, e) under q_0 .. q_{limbs_out-1}: shape
+    (B, 2, limbs_out, N).  a_ntt (B, limbs_out, N) and e (B, N) are the fresh
+    randomness (inputs).
+    """
+    ct = np.asarray(ct)
+    B = ct.shape[0]
+    Q2 = qs[0] * qs[1]
+    out = np.empty((B, 2, limbs_out, 1 << log_n), dtype=np.uint64)
+    for b in range(B):
+        res = decrypt_residues(ct[b, :, :2], s, qs[:2], psis[:2], log_n)
+        m = [centre(c, Q2) for c in crt_lift(res, qs[:2])]
+        out[b] = encrypt(m, s, np.asarray(a_ntt)[b], np.asarray(e)[b], qs[:limbs_out], psis[:limbs_out], log_n)
+    return out
