@@ -160,6 +160,46 @@ int ckks_rescale(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t* ct_out,
                  uint32_t count, uint32_t limbs, void* workspace, size_t workspace_bytes,
                  void* stream);
 
+/* Symmetric RLWE encryption, decryption and decrypt-then-encrypt refresh,
+ * batched.  In the paper these are the steps on the trusted side of each
+ * accelerator call (section 3.2: decrypt-compute-encrypt windows and the DtE
+ * refresh ct' = Enc(Dec(ct)); section 4.2 quotes about 30 ms each for the
+ * CPU-side encrypt and decrypt of one call).  They take the secret key as an
+ * input buffer, so calling them on a device puts that device inside the
+ * trust boundary: they serve deployments where it is (a trusted
+ * accelerator) and the generation and checking of encrypted workloads.
+ *   s_ntt  device uint32 [limbs][N]: the secret (ternary, or any integer
+ *          polynomial) reduced mod q_l and taken to NTT form (ckks_ntt).
+ *   a      device uint32 [count][limbs][N]: fresh uniform residues, NTT form.
+ *   e      device int32 [count][N]: fresh error coefficients, |e| < q_l.
+ * Encryption, per limb:  c0 = pt + NTT(e) - a (.) s,  c1 = a.
+ *   pt     device uint32 [count][limbs][N] (NTT form, e.g. ckks_linear_encode_poly
+ *          output), or NULL for a zero plaintext.
+ *   ct     device uint32 [count][2][limbs][N]; must not overlap the inputs. */
+int ckks_encrypt(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* s_ntt,
+                 const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs,
+                 uint32_t* ct, void* stream);
+
+/* Decryption to coefficient residues:  m[c][l] = INTT(c0 + c1 (.) s) mod q_l.
+ *   ct  device uint32 [count][2][limbs][N];  m  device uint32 [count][limbs][N]
+ *   (must not overlap ct).  Lifting to integers (CRT) and decoding are the
+ *   caller's. */
+int ckks_decrypt(const ckks_ctx* ctx, const uint32_t* ct, const uint32_t* s_ntt,
+                 uint32_t count, uint32_t limbs, uint32_t* m, void* stream);
+
+/* Decrypt-then-encrypt refresh (the DtE equation of section 3.2): the integer
+ * plaintext polynomial of ct_in is recovered from limbs 0 and 1 (CRT over
+ * q_0 q_1, centred; exact while every coefficient of the decrypted polynomial
+ * is below q_0 q_1 / 2 in magnitude, about 2^59) and encrypted afresh with
+ * (a, e) under limbs_out limbs.  The scale is unchanged (the caller carries it).
+ *   ct_in   device uint32 [count][2][limbs_in][N], 2 <= limbs_in <= L.
+ *   s_ntt   [limbs_out][N] (limbs_out >= 2);  a [count][limbs_out][N];  e [count][N].
+ *   ct_out  device uint32 [count][2][limbs_out][N], 2 <= limbs_out <= L; must
+ *           not overlap ct_in (its c1 rows serve as scratch during the call). */
+int ckks_refresh(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t limbs_in,
+                 const uint32_t* s_ntt, const uint32_t* a, const int32_t* e, uint32_t count,
+                 uint32_t limbs_out, uint32_t* ct_out, void* stream);
+
 /* Workspace size in bytes for `op` (ckks_op) with the given sizes; 0 when
  * none is needed; (size_t)-1 for an invalid request. */
 size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b,

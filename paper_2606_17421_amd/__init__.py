@@ -54,6 +54,9 @@ _SIGS = {
     "ckks_linear_mac_scalar": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp, _sz, _vp]),
     "ckks_linear_mac_poly": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp]),
     "ckks_rescale": (_i32, [_vp, _vp, _vp, _u32, _u32, _vp, _sz, _vp]),
+    "ckks_encrypt": (_i32, [_vp, _vp, _vp, _vp, _vp, _u32, _u32, _vp, _vp]),
+    "ckks_decrypt": (_i32, [_vp, _vp, _vp, _u32, _u32, _vp, _vp]),
+    "ckks_refresh": (_i32, [_vp, _vp, _u32, _vp, _vp, _vp, _u32, _u32, _vp, _vp]),
     "ckks_workspace_bytes": (_sz, [_vp, _i32, _u32, _u32, _u32]),
     "ckks_rescaled_scale": (_dbl, [_vp, _dbl, _u32]),
     "ckks_last_error": (ctypes.c_char_p, []),
@@ -212,6 +215,32 @@ def ckks_rescale(ctx: Context, ct_in, ct_out, count: int, limbs: int, workspace=
         ctx.handle, _ptr(ct_in, "ct_in", count * 2 * limbs * ctx.n * 4, 4),
         _ptr(ct_out, "ct_out", count * 2 * (limbs - 1) * ctx.n * 4, 4), count, limbs, ws, workspace_bytes,
         _stream(stream)), "ckks_rescale")
+
+
+def ckks_encrypt(ctx: Context, pt, s_ntt, a, e, count: int, limbs: int, ct, stream=None) -> None:
+    """pt may be None (zero plaintext); e holds int32 error coefficients [count][N]."""
+    rows = count * limbs * ctx.n * 4
+    _check(_lib.ckks_encrypt(
+        ctx.handle, _ptr(pt, "pt", rows, 4, True), _ptr(s_ntt, "s_ntt", limbs * ctx.n * 4 if count else 0, 4),
+        _ptr(a, "a", rows, 4), _ptr(e, "e", count * ctx.n * 4, 4), count, limbs, _ptr(ct, "ct", 2 * rows, 4),
+        _stream(stream)), "ckks_encrypt")
+
+
+def ckks_decrypt(ctx: Context, ct, s_ntt, count: int, limbs: int, m, stream=None) -> None:
+    rows = count * limbs * ctx.n * 4
+    _check(_lib.ckks_decrypt(
+        ctx.handle, _ptr(ct, "ct", 2 * rows, 4), _ptr(s_ntt, "s_ntt", limbs * ctx.n * 4 if count else 0, 4),
+        count, limbs, _ptr(m, "m", rows, 4), _stream(stream)), "ckks_decrypt")
+
+
+def ckks_refresh(ctx: Context, ct_in, limbs_in: int, s_ntt, a, e, count: int, limbs_out: int, ct_out,
+                 stream=None) -> None:
+    n4 = ctx.n * 4
+    _check(_lib.ckks_refresh(
+        ctx.handle, _ptr(ct_in, "ct_in", count * 2 * limbs_in * n4, 4), limbs_in,
+        _ptr(s_ntt, "s_ntt", max(limbs_out, 2) * n4 if count else 0, 4), _ptr(a, "a", count * limbs_out * n4, 4),
+        _ptr(e, "e", count * n4, 4), count, limbs_out, _ptr(ct_out, "ct_out", count * 2 * limbs_out * n4, 4),
+        _stream(stream)), "ckks_refresh")
 
 
 def ckks_rescaled_scale(ctx: Context, scale_in: float, limbs: int) -> float:

@@ -536,6 +536,81 @@ int ckks_rescale(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t* ct_out, u
   return e == hipSuccess ? ok() : hip_fail(e, "rescale launch");
 }
 
+// Rows handed to the batched transforms must keep their grids below 2^31
+// workgroups (64 per row in the N = 2^16 block pass).
+static int check_rows(const ckks_ctx* ctx, uint32_t count, uint32_t limbs) {
+  const size_t rows = static_cast<size_t>(count) * limbs;
+  if (rows > 0x7FFFFFFFull / (ctx->log_n == 16 ? 64 : 1))
+    return fail(CKKS_E_INVALID_ARG, "too many polynomials (%zu rows)", rows);
+  return CKKS_OK;
+}
+
+static bool overlaps(const void* x, size_t xb, const void* y, size_t yb) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(x), b0 = reinterpret_cast<uintptr_t>(y);
+  return a0 < b0 + yb && b0 < a0 + xb;
+}
+
+int ckks_encrypt(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* s_ntt, const uint32_t* a,
+                 const int32_t* e, uint32_t count, uint32_t limbs, uint32_t* ct, void* stream) {
+  if (int rc = check_ctx(ctx)) return rc;
+  if (int rc = check_limbs(ctx, limbs, 1)) return rc;
+  if (count == 0) return ok();
+  if (int rc = check_rows(ctx, count, limbs)) return rc;
+  if (int rc = check_ptr(s_ntt, "s_ntt")) return rc;
+  if (int rc = check_ptr(a, "a")) return rc;
+  if (int rc = check_ptr(e, "e")) return rc;
+  if (int rc = check_ptr(ct, "ct")) return rc;
+  if (pt && !aligned16(pt)) return fail(CKKS_E_INVALID_ARG, "pt is not 16-byte aligned");
+  const size_t n = ctx->n, ct_bytes = size_t(count) * 2 * limbs * n * 4;
+  if (overlaps(ct, ct_bytes, a, size_t(count) * limbs * n * 4) || overlaps(ct, ct_bytes, e, size_t(count) * n * 4) ||
+      overlaps(ct, ct_bytes, s_ntt, size_t(limbs) * n * 4) || (pt && overlaps(ct, ct_bytes, pt, size_t(count) * limbs * n * 4)))
+    return fail(CKKS_E_INVALID_ARG, "ct overlaps an input");
+  DeviceGuard guard(ctx->device);
+  hipError_t he = ckks::launch_encrypt(ctx->t, pt, s_ntt, a, e, count, limbs, ct, static_cast<hipStream_t>(stream));
+  return he == hipSuccess ? ok() : hip_fail(he, "encrypt launch");
+}
+
+int ckks_decrypt(const ckks_ctx* ctx, const uint32_t* ct, const uint32_t* s_ntt, uint32_t count, uint32_t limbs,
+                 uint32_t* m, void* stream) {
+  if (int rc = check_ctx(ctx)) return rc;
+  if (int rc = check_limbs(ctx, limbs, 1)) return rc;
+  if (count == 0) return ok();
+  if (int rc = check_rows(ctx, count, limbs)) return rc;
+  if (int rc = check_ptr(ct, "ct")) return rc;
+  if (int rc = check_ptr(s_ntt, "s_ntt")) return rc;
+  if (int rc = check_ptr(m, "m")) return rc;
+  const size_t n = ctx->n;
+  if (overlaps(m, size_t(count) * limbs * n * 4, ct, size_t(count) * 2 * limbs * n * 4))
+    return fail(CKKS_E_INVALID_ARG, "m overlaps ct");
+  DeviceGuard guard(ctx->device);
+  hipError_t he = ckks::launch_decrypt(ctx->t, ct, s_ntt, count, limbs, m, static_cast<hipStream_t>(stream));
+  return he == hipSuccess ? ok() : hip_fail(he, "decrypt launch");
+}
+
+int ckks_refresh(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
+                 const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out, uint32_t* ct_out,
+                 void* stream) {
+  if (int rc = check_ctx(ctx)) return rc;
+  if (int rc = check_limbs(ctx, limbs_in, 2)) return rc;
+  if (int rc = check_limbs(ctx, limbs_out, 2)) return rc;
+  if (count == 0) return ok();
+  if (int rc = check_rows(ctx, count, limbs_in > limbs_out ? limbs_in : limbs_out)) return rc;
+  if (int rc = check_ptr(ct_in, "ct_in")) return rc;
+  if (int rc = check_ptr(s_ntt, "s_ntt")) return rc;
+  if (int rc = check_ptr(a, "a")) return rc;
+  if (int rc = check_ptr(e, "e")) return rc;
+  if (int rc = check_ptr(ct_out, "ct_out")) return rc;
+  const size_t n = ctx->n, out_bytes = size_t(count) * 2 * limbs_out * n * 4;
+  if (overlaps(ct_out, out_bytes, ct_in, size_t(count) * 2 * limbs_in * n * 4) ||
+      overlaps(ct_out, out_bytes, a, size_t(count) * limbs_out * n * 4) ||
+      overlaps(ct_out, out_bytes, e, size_t(count) * n * 4) || overlaps(ct_out, out_bytes, s_ntt, size_t(limbs_out) * n * 4))
+    return fail(CKKS_E_INVALID_ARG, "ct_out overlaps an input");
+  DeviceGuard guard(ctx->device);
+  hipError_t he = ckks::launch_refresh(ctx->t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out,
+                                       static_cast<hipStream_t>(stream));
+  return he == hipSuccess ? ok() : hip_fail(he, "refresh launch");
+}
+
 size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b, uint32_t limbs) {
   if (!ctx || limbs < 1 || limbs > ctx->L) return static_cast<size_t>(-1);
   switch (op) {

@@ -96,9 +96,11 @@ __device__ __forceinline__ uint32_t reduce_f64_int(double v, uint32_t q, double 
 // Launchers (each returns hipSuccess or the launch error)
 // ---------------------------------------------------------------------------
 
-// In-place forward / inverse NTT of rows[count_rows][N]; row r uses limb r % limbs.
+// In-place forward / inverse NTT of count_rows rows; logical row r uses limb
+// r % limbs and is physical row (r / limbs) * gstride + r % limbs of
+// rows[][N] (gstride 0 means limbs: packed [count][limbs][N]).
 hipError_t launch_ntt(const Tables& t, uint32_t* rows, size_t count_rows, uint32_t limbs,
-                      bool inverse, hipStream_t s);
+                      bool inverse, hipStream_t s, uint32_t gstride = 0);
 
 hipError_t launch_encode_scalar(const Tables& t, const double* w, size_t count, uint32_t limbs,
                                 double scale, uint32_t* w_enc, hipStream_t s);
@@ -126,5 +128,14 @@ hipError_t launch_rescale(const Tables& t, const uint32_t* ct_in, uint32_t* ct_o
                           uint32_t limbs, void* workspace, hipStream_t s);
 
 hipError_t launch_zero(uint32_t* p, size_t words, hipStream_t s);
+
+// Symmetric RLWE over ciphertexts [count][2][limbs][N], NTT form (rlwe.hip).
+hipError_t launch_encrypt(const Tables& t, const uint32_t* pt, const uint32_t* s_ntt, const uint32_t* a,
+                          const int32_t* e, uint32_t count, uint32_t limbs, uint32_t* ct, hipStream_t s);
+hipError_t launch_decrypt(const Tables& t, const uint32_t* ct, const uint32_t* s_ntt, uint32_t count,
+                          uint32_t limbs, uint32_t* m, hipStream_t s);
+hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
+                          const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
+                          uint32_t* ct_out, hipStream_t s);
 
 }  // namespace ckks

@@ -6,21 +6,30 @@
 // N = 2^16 (256 KiB per row, above the 160 KiB LDS): two passes over HBM,
 // a column pass over the top 6 index bits (64 residues per thread, twiddles
 // uniform across the workgroup) and a block pass over 1024-point blocks.
+//
+// Logical row r uses limb r % limbs and lives at physical row
+// (r / limbs) * gstride + r % limbs: gstride = limbs for packed
+// [count][limbs][N] rows, 2 * limbs for one component of [count][2][limbs][N]
+// ciphertexts.
 #include "ntt_core.hpp"
 
 namespace ckks {
 namespace {
 
+__device__ __forceinline__ size_t phys_row(size_t r, uint32_t limbs, uint32_t gstride) {
+  return (r / limbs) * gstride + r % limbs;
+}
+
 template <int LOGN, bool INV>
 __global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSimd) void ntt_whole_kernel(Tables tb, uint32_t* rows,
-                                                                          uint32_t limbs) {
+                                                                          uint32_t limbs, uint32_t gstride) {
   using P = typename WholePlan<LOGN>::P;
   constexpr int LOGE = WholePlan<LOGN>::LOGE;
   __shared__ uint32_t lds[P::lds_words];
   const size_t r = blockIdx.x;
   const uint32_t l = static_cast<uint32_t>(r % limbs);
   const uint32_t t = threadIdx.x;
-  uint32_t* a = rows + r * P::B;
+  uint32_t* a = rows + phys_row(r, limbs, gstride) * P::B;
   const uint32_t q = tb.q[l];
   const size_t toff = static_cast<size_t>(l) << LOGN;
   uint32_t v[P::E];
@@ -50,13 +59,13 @@ constexpr int kColThreads = 256;
 
 template <bool INV>
 __global__ __launch_bounds__(kColThreads) void ntt16_cols_kernel(Tables tb, uint32_t* rows,
-                                                                 uint32_t limbs) {
+                                                                 uint32_t limbs, uint32_t gstride) {
   using P = Plan<16, kColLogE>;
   constexpr int kColsPerRow = 1 << (16 - kColLogE);
   const size_t r = blockIdx.x / (kColsPerRow / kColThreads);
   const uint32_t c = (blockIdx.x % (kColsPerRow / kColThreads)) * kColThreads + threadIdx.x;
   const uint32_t l = static_cast<uint32_t>(r % limbs);
-  uint32_t* a = rows + (r << 16);
+  uint32_t* a = rows + (phys_row(r, limbs, gstride) << 16);
   const uint32_t q = tb.q[l];
   const size_t toff = static_cast<size_t>(l) << 16;
   uint32_t v[P::E];
@@ -81,7 +90,8 @@ constexpr int kBlkLogE = 4;
 template <bool INV>
 __global__ __launch_bounds__(1 << (kBlkLogB - kBlkLogE)) void ntt16_blocks_kernel(Tables tb,
                                                                                  uint32_t* rows,
-                                                                                 uint32_t limbs) {
+                                                                                 uint32_t limbs,
+                                                                                 uint32_t gstride) {
   using P = Plan<kBlkLogB, kBlkLogE>;
   __shared__ uint32_t lds[P::lds_words];
   constexpr int kBlocksPerRow = 1 << (16 - kBlkLogB);
@@ -89,7 +99,7 @@ __global__ __launch_bounds__(1 << (kBlkLogB - kBlkLogE)) void ntt16_blocks_kerne
   const uint32_t blk = blockIdx.x % kBlocksPerRow;
   const uint32_t l = static_cast<uint32_t>(r % limbs);
   const uint32_t t = threadIdx.x;
-  uint32_t* a = rows + (r << 16) + (static_cast<size_t>(blk) << kBlkLogB);
+  uint32_t* a = rows + (phys_row(r, limbs, gstride) << 16) + (static_cast<size_t>(blk) << kBlkLogB);
   const uint32_t q = tb.q[l];
   const size_t toff = static_cast<size_t>(l) << 16;
   uint32_t v[P::E];
@@ -112,26 +122,26 @@ __global__ __launch_bounds__(1 << (kBlkLogB - kBlkLogE)) void ntt16_blocks_kerne
 
 template <int LOGN>
 hipError_t launch_whole(const Tables& t, uint32_t* rows, size_t count, uint32_t limbs, bool inv,
-                        hipStream_t s) {
+                        hipStream_t s, uint32_t gs) {
   using P = typename WholePlan<LOGN>::P;
   if (inv)
-    ntt_whole_kernel<LOGN, true><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs);
+    ntt_whole_kernel<LOGN, true><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs, gs);
   else
-    ntt_whole_kernel<LOGN, false><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs);
+    ntt_whole_kernel<LOGN, false><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs, gs);
   return hipGetLastError();
 }
 
 hipError_t launch_ntt16(const Tables& t, uint32_t* rows, size_t count, uint32_t limbs, bool inv,
-                        hipStream_t s) {
+                        hipStream_t s, uint32_t gs) {
   const uint32_t col_grid = static_cast<uint32_t>(count * ((1 << (16 - kColLogE)) / kColThreads));
   const uint32_t blk_grid = static_cast<uint32_t>(count * (1 << (16 - kBlkLogB)));
   constexpr int blk_threads = 1 << (kBlkLogB - kBlkLogE);
   if (!inv) {
-    ntt16_cols_kernel<false><<<col_grid, kColThreads, 0, s>>>(t, rows, limbs);
-    ntt16_blocks_kernel<false><<<blk_grid, blk_threads, 0, s>>>(t, rows, limbs);
+    ntt16_cols_kernel<false><<<col_grid, kColThreads, 0, s>>>(t, rows, limbs, gs);
+    ntt16_blocks_kernel<false><<<blk_grid, blk_threads, 0, s>>>(t, rows, limbs, gs);
   } else {
-    ntt16_blocks_kernel<true><<<blk_grid, blk_threads, 0, s>>>(t, rows, limbs);
-    ntt16_cols_kernel<true><<<col_grid, kColThreads, 0, s>>>(t, rows, limbs);
+    ntt16_blocks_kernel<true><<<blk_grid, blk_threads, 0, s>>>(t, rows, limbs, gs);
+    ntt16_cols_kernel<true><<<col_grid, kColThreads, 0, s>>>(t, rows, limbs, gs);
   }
   return hipGetLastError();
 }
@@ -139,16 +149,17 @@ hipError_t launch_ntt16(const Tables& t, uint32_t* rows, size_t count, uint32_t 
 }  // namespace
 
 hipError_t launch_ntt(const Tables& t, uint32_t* rows, size_t count_rows, uint32_t limbs,
-                      bool inverse, hipStream_t s) {
+                      bool inverse, hipStream_t s, uint32_t gstride) {
   if (count_rows == 0) return hipSuccess;
+  const uint32_t gs = gstride ? gstride : limbs;
   switch (t.log_n) {
-    case 10: return launch_whole<10>(t, rows, count_rows, limbs, inverse, s);
-    case 11: return launch_whole<11>(t, rows, count_rows, limbs, inverse, s);
-    case 12: return launch_whole<12>(t, rows, count_rows, limbs, inverse, s);
-    case 13: return launch_whole<13>(t, rows, count_rows, limbs, inverse, s);
-    case 14: return launch_whole<14>(t, rows, count_rows, limbs, inverse, s);
-    case 15: return launch_whole<15>(t, rows, count_rows, limbs, inverse, s);
-    case 16: return launch_ntt16(t, rows, count_rows, limbs, inverse, s);
+    case 10: return launch_whole<10>(t, rows, count_rows, limbs, inverse, s, gs);
+    case 11: return launch_whole<11>(t, rows, count_rows, limbs, inverse, s, gs);
+    case 12: return launch_whole<12>(t, rows, count_rows, limbs, inverse, s, gs);
+    case 13: return launch_whole<13>(t, rows, count_rows, limbs, inverse, s, gs);
+    case 14: return launch_whole<14>(t, rows, count_rows, limbs, inverse, s, gs);
+    case 15: return launch_whole<15>(t, rows, count_rows, limbs, inverse, s, gs);
+    case 16: return launch_ntt16(t, rows, count_rows, limbs, inverse, s, gs);
     default: return hipErrorInvalidValue;
   }
 }

@@ -20,7 +20,8 @@ def _declared():
 def test_header_declares_the_boundary():
     names = _declared()
     for must in ("ckks_ntt", "ckks_intt", "ckks_linear_encode_scalar", "ckks_linear_encode_poly",
-                 "ckks_linear_mac_scalar", "ckks_linear_mac_poly", "ckks_rescale"):
+                 "ckks_linear_mac_scalar", "ckks_linear_mac_poly", "ckks_rescale",
+                 "ckks_encrypt", "ckks_decrypt", "ckks_refresh"):
         assert must in names
 
 
@@ -39,6 +40,9 @@ def test_null_context_is_rejected_without_a_gpu():
     assert "null context" in ck.ckks_last_error()
     assert lib.ckks_rescale(None, None, None, 1, 2, None, 0, None) == ck.CKKS_E_INVALID_ARG
     assert lib.ckks_workspace_bytes(None, ck.CKKS_OP_RESCALE, 1, 0, 2) == ctypes.c_size_t(-1).value
+    assert lib.ckks_encrypt(None, None, None, None, None, 1, 1, None, None) == ck.CKKS_E_INVALID_ARG
+    assert lib.ckks_decrypt(None, None, None, 1, 1, None, None) == ck.CKKS_E_INVALID_ARG
+    assert lib.ckks_refresh(None, None, 2, None, None, None, 1, 2, None, None) == ck.CKKS_E_INVALID_ARG
     h = ctypes.c_void_p()
     assert lib.ckks_ctx_create(ctypes.byref(h), 9, 2, None, 0) == ck.CKKS_E_INVALID_ARG      # log_n < 10
     assert lib.ckks_ctx_create(ctypes.byref(h), 14, 17, None, 0) == ck.CKKS_E_INVALID_ARG    # too many limbs
