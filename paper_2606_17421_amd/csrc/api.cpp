@@ -234,6 +234,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   std::vector<uint32_t> fwd(size_t(L) * n), fwds(size_t(L) * n), inv(size_t(L) * n), invs(size_t(L) * n);
   std::vector<uint32_t> ninv(L), ninvs(L), qinv(size_t(L) * L, 0), qinvs(size_t(L) * L, 0);
   std::vector<double> qrec(L);
+  std::vector<uint32_t> bar(L);
   std::vector<uint32_t> p256(size_t(L) * 8);
   for (uint32_t l = 0; l < L; ++l) {
     const uint64_t q = c->q[l];
@@ -255,6 +256,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
     ninv[l] = static_cast<uint32_t>(powmod(n, q - 2, q));
     ninvs[l] = shoup(ninv[l], c->q[l]);
     qrec[l] = 1.0 / static_cast<double>(q);
+    bar[l] = static_cast<uint32_t>((uint64_t(1) << 61) / q);
     uint64_t pw = 1;
     for (int e = 0; e < 8; ++e) {
       p256[size_t(l) * 8 + e] = static_cast<uint32_t>(pw);
@@ -279,6 +281,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   const size_t o_qinv = blob.add(qinv.data(), qinv.size() * 4);
   const size_t o_qinvs = blob.add(qinvs.data(), qinvs.size() * 4);
   const size_t o_qrec = blob.add(qrec.data(), L * 8);
+  const size_t o_bar = blob.add(bar.data(), L * 4);
   const size_t o_p256 = blob.add(p256.data(), p256.size() * 4);
   size_t o_perm = 0, o_fft = 0, o_rfft = 0, o_dct = 0;
   const bool enc = log_n <= 15;
@@ -350,6 +353,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   t.qinv = reinterpret_cast<const uint32_t*>(base + o_qinv);
   t.qinv_shoup = reinterpret_cast<const uint32_t*>(base + o_qinvs);
   t.q_recip = reinterpret_cast<const double*>(base + o_qrec);
+  t.barrett = reinterpret_cast<const uint32_t*>(base + o_bar);
   t.pow256 = reinterpret_cast<const uint32_t*>(base + o_p256);
   if (enc) {
     t.slot_perm = reinterpret_cast<const uint32_t*>(base + o_perm);

@@ -30,6 +30,7 @@ struct Tables {
   const uint32_t* qinv;        // [L][L]  qinv[m*L + l] = q_m^-1 mod q_l (0 on the diagonal)
   const uint32_t* qinv_shoup;  // [L][L]
   const double* q_recip;       // [L]     1.0 / q_l rounded to nearest
+  const uint32_t* barrett;     // [L]     floor(2^61 / q_l) (< 2^32 for q_l > 2^29)
   const uint32_t* pow256;      // [L][8]  256^s mod q_l, s < 8
   // Encode tables (present when log_n <= 15; M = N/2, P = N/4).
   const uint32_t* slot_perm;   // [M]  slot index j whose odd exponent is 2u+1 (up to sign)
@@ -64,6 +65,18 @@ __device__ __forceinline__ uint32_t add_mod(uint32_t a, uint32_t b, uint32_t q) 
 __device__ __forceinline__ uint32_t sub_mod(uint32_t a, uint32_t b, uint32_t q) {
   uint32_t d = a - b + q;
   return min(d, d - q);
+}
+
+// a * b mod q for a < 2^30, b < q, with mu = floor(2^61 / q) (Barrett, 32-bit
+// operations only).  With x = a b < 2^60, t = floor(x / 2^29) and qt =
+// floor(t mu / 2^32), x/q - 2 < qt <= x/q, so x - qt q lies in [0, 3q) and its
+// low 32 bits are exact (3q < 2^32); two conditional subtractions finish.
+__device__ __forceinline__ uint32_t mul_mod_barrett(uint32_t a, uint32_t b, uint32_t q, uint32_t mu) {
+  const uint32_t lo = a * b, hi = __umulhi(a, b);
+  const uint32_t t = __builtin_amdgcn_alignbit(hi, lo, 29);  // bits 29..60 of a b
+  uint32_t r = lo - __umulhi(t, mu) * q;
+  r = min(r, r - q);
+  return min(r, r - q);
 }
 
 // x mod q for any x < 2^64, with qr = 1.0/q.  The fp64 quotient estimate is

@@ -11,11 +11,11 @@
 // coefficients lie within q0 q1 / 2 in magnitude) and encrypted afresh under
 // limbs_out limbs.
 //
-// The transforms are the batched NTT kernels, run over the c0 rows (or a
-// pair of scratch rows) of the ciphertext buffer through their row-group
-// stride; the kernels here are the pointwise passes around them, 16 bytes
-// per thread and limb.
-#include "ckks_internal.hpp"
+// Encryption and decryption run the batched NTT kernels over the c0 rows (or
+// the output rows) through their row-group stride, with pointwise passes
+// around them, 16 bytes per thread and limb.  The refresh is one fused kernel
+// per ciphertext up to N = 2^14 and the same pass structure above.
+#include "ntt_core.hpp"
 
 namespace ckks {
 namespace {
@@ -31,16 +31,17 @@ __device__ __forceinline__ v4u ld4(const uint32_t* p) { return *reinterpret_cast
 __device__ __forceinline__ v4s ld4(const int32_t* p) { return *reinterpret_cast<const v4s*>(p); }
 __device__ __forceinline__ void st4(uint32_t* p, v4u v) { *reinterpret_cast<v4u*>(p) = v; }
 
-// a * b mod q for residues a, b < q.
-__device__ __forceinline__ uint32_t mul_mod(uint32_t a, uint32_t b, uint32_t q, double qr) {
-  return reduce_u64(static_cast<uint64_t>(a) * b, q, qr);
-}
-
 // Signed 64-bit x mod q, in [0, q).
 __device__ __forceinline__ uint32_t reduce_i64(int64_t x, uint32_t q, double qr) {
   const uint64_t ax = static_cast<uint64_t>(x < 0 ? -x : x);
   const uint32_t r = reduce_u64(ax, q, qr);
   return (x < 0 && r != 0) ? q - r : r;
+}
+
+// Buffer resource over one row of N words (row bases live in scalar
+// registers; per-lane offsets and per-element constants index into it).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* base, uint32_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, n * 4, 0x00020000);
 }
 
 // Thread -> (ciphertext c, coefficient quad k4) over count * N/4 quads.
@@ -85,8 +86,7 @@ __global__ __launch_bounds__(kThreads) void enc_combine_kernel(Tables tb, const 
   const Quad p = quad_of(n, count);
   if (!p.ok) return;
   for (uint32_t l = 0; l < limbs; ++l) {
-    const uint32_t q = tb.q[l];
-    const double qr = tb.q_recip[l];
+    const uint32_t q = tb.q[l], mu = tb.barrett[l];
     const size_t row = (p.c * limbs + l) * n + p.k;
     uint32_t* c0p = ct + ((p.c * 2) * limbs + l) * n + p.k;
     uint32_t* c1p = c0p + static_cast<size_t>(limbs) * n;
@@ -96,7 +96,7 @@ __global__ __launch_bounds__(kThreads) void enc_combine_kernel(Tables tb, const 
     const v4u pv = pt ? ld4(pt + row) : v4u{0, 0, 0, 0};
     v4u o;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = sub_mod(add_mod(c0[j], pv[j], q), mul_mod(av[j], sv[j], q, qr), q);
+    for (int j = 0; j < 4; ++j) o[j] = sub_mod(add_mod(c0[j], pv[j], q), mul_mod_barrett(av[j], sv[j], q, mu), q);
     st4(c0p, o);
     st4(c1p, av);
   }
@@ -113,15 +113,14 @@ __global__ __launch_bounds__(kThreads) void dec_pointwise_kernel(Tables tb, cons
   const Quad p = quad_of(n, count);
   if (!p.ok) return;
   for (uint32_t l = 0; l < limbs_used; ++l) {
-    const uint32_t q = tb.q[l];
-    const double qr = tb.q_recip[l];
+    const uint32_t q = tb.q[l], mu = tb.barrett[l];
     const uint32_t* c0p = ct + ((p.c * 2) * ct_limbs + l) * n + p.k;
     const v4u c0 = ld4(c0p);
     const v4u c1 = ld4(c0p + static_cast<size_t>(ct_limbs) * n);
     const v4u sv = ld4(s_ntt + static_cast<size_t>(l) * n + p.k);
     v4u o;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = add_mod(c0[j], mul_mod(c1[j], sv[j], q, qr), q);
+    for (int j = 0; j < 4; ++j) o[j] = add_mod(c0[j], mul_mod_barrett(c1[j], sv[j], q, mu), q);
     st4(out + (p.c * out_gstride + out_off + l) * n + p.k, o);
   }
 }
@@ -163,6 +162,116 @@ __global__ __launch_bounds__(kThreads) void dte_lift_kernel(Tables tb, const int
   }
 }
 
+// Fused refresh for N <= 2^14: one workgroup per ciphertext.  Limbs 0 and
+// 1 of c0 + c1 (.) s are read coalesced and inverse-transformed in LDS; the
+// CRT value over q0 q1 is kept as its two digits x = x0 + q0 k (k with the
+// centring flag in bit 31) in the group-0 layout that the forward transform
+// starts from, and per output limb it is rebuilt mod q_l with 32-bit
+// Barrett products, the fresh error added, transformed, combined with a and
+// s and written coalesced.  Row transfers per ciphertext: 4 + limbs_out (a)
+// + limbs_out (error, L2) in, 2 limbs_out out; the multi-pass route moves
+// 13 + 7 limbs_out.
+// 16 residues per thread up to 2^14 (1024 threads) keeps the live state in
+// registers.
+template <int LOGN>
+struct RefreshPlan {
+  static_assert(LOGN <= 14, "the fused refresh serves N <= 2^14");
+  static constexpr int LOGE = 4;
+  using P = Plan<LOGN, LOGE>;
+  static constexpr int kWavesPerSimd = 4;
+};
+
+template <int LOGN>
+__global__ __launch_bounds__(RefreshPlan<LOGN>::P::T, RefreshPlan<LOGN>::kWavesPerSimd) void refresh_kernel(
+    Tables tb, const uint32_t* __restrict__ ct_in, uint32_t limbs_in, const uint32_t* __restrict__ s_ntt,
+    const uint32_t* __restrict__ a, const int32_t* __restrict__ e, uint32_t limbs_out,
+    uint32_t* __restrict__ ct_out) {
+  using P = typename RefreshPlan<LOGN>::P;
+  constexpr int LOGE = RefreshPlan<LOGN>::LOGE;
+  constexpr int N = P::B;
+  __shared__ uint32_t lds[P::lds_words];
+  const size_t c = blockIdx.x;
+  const uint32_t t = threadIdx.x;
+  const uint32_t vofs = pos_coalesced<LOGE>(t, 0) * 4;  // byte offset of element 0 in the coalesced layout
+
+  uint32_t x0[P::E], v[P::E];
+#pragma unroll
+  for (int l = 0; l < 2; ++l) {
+    const uint32_t q = tb.q[l], mu = tb.barrett[l];
+    const auto r_c0 = row_rsrc(ct_in + ((c * 2) * limbs_in + l) * N, N);
+    const auto r_c1 = row_rsrc(ct_in + ((c * 2 + 1) * limbs_in + l) * N, N);
+    const auto r_s = row_rsrc(s_ntt + static_cast<size_t>(l) * N, N);
+    if (l == 1) __syncthreads();  // the last (workgroup-wide) exchange of limb 0 is read out
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) {
+      const uint32_t c0 = __builtin_amdgcn_raw_buffer_load_b32(r_c0, vofs, j << 8, 0);
+      const uint32_t c1 = __builtin_amdgcn_raw_buffer_load_b32(r_c1, vofs, j << 8, 0);
+      const uint32_t sv = __builtin_amdgcn_raw_buffer_load_b32(r_s, vofs, j << 8, 0);
+      v[j] = add_mod(c0, mul_mod_barrett(c1, sv, q, mu), q);
+    }
+    wave_relayout<LOGN, LOGE, true>(v, t, lds);
+    const size_t tl = static_cast<size_t>(l) << LOGN;
+    inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + tl, tb.inv_shoup + tl, q, lds);
+    const uint32_t ni = tb.ninv[l], nis = tb.ninv_shoup[l];
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) {
+      v[j] = mul_shoup(v[j], ni, nis, q);
+      if (l == 0) x0[j] = v[j];
+    }
+  }
+  // CRT digits: x = x0 + q0 k in [0, q0 q1), k = (r1 - r0) q0^-1 mod q1;
+  // bit 31 of kf marks x > q0 q1 / 2 (centred value x - q0 q1).
+  const uint32_t q0 = tb.q[0], q1 = tb.q[1];
+  const uint32_t w = tb.qinv[0 * tb.L + 1], ws = tb.qinv_shoup[0 * tb.L + 1];  // q0^-1 mod q1
+  const uint64_t half = static_cast<uint64_t>(q0) * q1 / 2;
+  uint32_t kf[P::E];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    const uint32_t r0m = x0[j] >= q1 ? x0[j] - q1 : x0[j];  // x0 < q0 < 2 q1
+    const uint32_t k = mul_shoup(sub_mod(v[j], r0m, q1), w, ws, q1);
+    const uint64_t x = static_cast<uint64_t>(x0[j]) + static_cast<uint64_t>(q0) * k;
+    kf[j] = k | (x > half ? 0x80000000u : 0u);
+  }
+  // the error row through a buffer resource: the per-j offsets j T are scalar constants
+  const auto er = row_rsrc(e + c * N, N);
+  for (uint32_t l = 0; l < limbs_out; ++l) {
+    const uint32_t q = tb.q[l], mu = tb.barrett[l];
+    const uint32_t q0l = q0 >= q ? q0 - q : q0, q1l = q1 >= q ? q1 - q : q1;  // q0, q1 < 2q
+    const uint32_t q2l = mul_mod_barrett(q0l, q1l, q, mu);                      // q0 q1 mod q
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) {
+      const uint32_t x0l = x0[j] >= q ? x0[j] - q : x0[j];
+      uint32_t y = add_mod(x0l, mul_mod_barrett(kf[j] & 0x7fffffffu, q0l, q, mu), q);
+      if (kf[j] >> 31) y = sub_mod(y, q2l, q);
+      const int32_t ev = static_cast<int32_t>(
+          __builtin_amdgcn_raw_buffer_load_b32(er, t * 4, P::template pos<0>(0, j) * 4, 0));
+      v[j] = ev < 0 ? sub_mod(y, static_cast<uint32_t>(-ev), q) : add_mod(y, static_cast<uint32_t>(ev), q);
+    }
+    const size_t tl = static_cast<size_t>(l) << LOGN;
+    fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+    wave_relayout<LOGN, LOGE, false>(v, t, lds);
+    const auto r_o0 = row_rsrc(ct_out + ((c * 2) * limbs_out + l) * N, N);
+    const auto r_o1 = row_rsrc(ct_out + ((c * 2 + 1) * limbs_out + l) * N, N);
+    const auto r_a = row_rsrc(a + (c * limbs_out + l) * N, N);
+    const auto r_s = row_rsrc(s_ntt + static_cast<size_t>(l) * N, N);
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) {
+      const uint32_t av = __builtin_amdgcn_raw_buffer_load_b32(r_a, vofs, j << 8, 0);
+      const uint32_t sv = __builtin_amdgcn_raw_buffer_load_b32(r_s, vofs, j << 8, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(sub_mod(v[j], mul_mod_barrett(av, sv, q, mu), q), r_o0, vofs, j << 8, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(av, r_o1, vofs, j << 8, 0);
+    }
+  }
+}
+
+template <int LOGN>
+hipError_t launch_refresh_fused(const Tables& t, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
+                                const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
+                                uint32_t* ct_out, hipStream_t s) {
+  refresh_kernel<LOGN><<<count, RefreshPlan<LOGN>::P::T, 0, s>>>(t, ct_in, limbs_in, s_ntt, a, e, limbs_out, ct_out);
+  return hipGetLastError();
+}
+
 uint32_t quad_grid(uint32_t n, uint32_t count) {
   const size_t quads = static_cast<size_t>(count) * (n / 4);
   return static_cast<uint32_t>((quads + kThreads - 1) / kThreads);
@@ -193,6 +302,16 @@ hipError_t launch_decrypt(const Tables& t, const uint32_t* ct, const uint32_t* s
 hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
                           const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
                           uint32_t* ct_out, hipStream_t s) {
+  switch (t.log_n) {  // one fused kernel up to 2^14
+    case 10: return launch_refresh_fused<10>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+    case 11: return launch_refresh_fused<11>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+    case 12: return launch_refresh_fused<12>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+    case 13: return launch_refresh_fused<13>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+    case 14: return launch_refresh_fused<14>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+    default: break;
+  }
+  // N >= 2^15: pointwise passes around the batched transforms (at 2^15 the
+  // fused kernel's 32 residues per thread would spill)
   const uint32_t grid = quad_grid(t.n, count);
   const uint32_t gs = 2 * limbs_out;
   // 1. limbs 0 and 1 of c0 + c1 (.) s into the c1 rows 0, 1 of ct_out (scratch), then INTT them
