@@ -23,6 +23,10 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build the HIP library first "
                       "(python paper_2606_17421_amd/build.py)")
 
+# torch (device memory and streams) brings its HIP runtime up first: loaded
+# before it, the library's runtime finds no devices in a later torch session.
+import torch  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 CKKS_OK = 0

@@ -1,0 +1,86 @@
+"""GPU execution of residency plans (section 3.3's pin / fallback-encode and
+refresh lines): the result does not depend on the budget, and the chain equals
+the oracle's composition of encode_poly, mac_poly, rescale and refresh."""
+import numpy as np
+import pytest
+
+from oracle import encode as OE
+from oracle import linear as OL
+from oracle import rlwe as OR
+from paper_2606_17421_amd.planner import Executor, LinearGroup, plan
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+LOG_N, L, SCALE = 10, 4, float(1 << 25)
+
+
+def model(d, layers):
+    return [LinearGroup(f"g{i}", d, d, tee_after=(i == 1)) for i in range(layers)]
+
+
+def secret_inputs(ck, ctx, d, seed):
+    qs, n = ctx.moduli, ctx.n
+    st = gen.streams(seed, LOG_N)
+    s = gen.ternary_secret(st["secret"], n)
+    s_res = np.stack([np.mod(s, q) for q in qs]).astype(np.uint32)
+    s_ntt = ck.to_device(s_res)
+    ck.ckks_ntt(ctx, s_ntt, 1, L)
+    a = gen.uniform_residues(st["residues"], (d,), qs, n)
+    e = gen.gaussian_error(st["error"], (d, n)).astype(np.int32)
+    ct = gen.uniform_residues(st["residues"], (d, 2), qs, n)
+    return s, a, e, ct, {"s_ntt": s_ntt, "a": ck.to_device(a), "e": ck.to_device(e)}
+
+
+def run(ck, ctx, groups, budget, weights_dev, sec, ct_dev):
+    p = plan(groups, budget, L, ctx.n)
+    ex = Executor(ctx, p, weights_dev, SCALE, sec)
+    out, limbs = ex.run(ct_dev)
+    d = groups[-1].d_out
+    return p, ck.to_host_u32(out[: d * 2 * limbs * ctx.n]).reshape(d, 2, limbs, ctx.n)
+
+
+def test_result_does_not_depend_on_the_budget(gpu_lib):
+    ck = gpu_lib
+    ctx = ck.Context(LOG_N, L)
+    d, layers = 8, 5
+    groups = model(d, layers)
+    st = gen.streams(501, LOG_N)
+    W = [gen.poly_weights(st["weights"], d, d, ctx.n // 2).reshape(d * d, ctx.n // 2) for _ in range(layers)]
+    Wd = [ck.to_device(np.ascontiguousarray(w)) for w in W]
+    s, a, e, ct, sec = secret_inputs(ck, ctx, d, 502)
+    ct_dev = ck.to_device(ct)
+    full = plan(groups, 1 << 40, L, ctx.n)
+    outs = {}
+    for budget in (1 << 40, 0, full.steps[0].encoded_bytes + full.steps[1].encoded_bytes):
+        p, outs[budget] = run(ck, ctx, groups, budget, Wd, sec, ct_dev)
+        assert p.pinned + p.fallback == layers
+    ref = outs[1 << 40]
+    for budget, o in outs.items():
+        assert np.array_equal(o, ref), budget
+    assert plan(groups, 0, L, ctx.n).fallback == layers
+
+
+def test_chain_equals_the_oracle_composition(gpu_lib):
+    """Constant-slot weights encode exactly on both sides (the constant polynomial
+    round(c scale)), so the GPU chain is compared with the oracle bit for bit."""
+    ck = gpu_lib
+    ctx = ck.Context(LOG_N, L)
+    qs, psis, n = ctx.moduli, ctx.roots, ctx.n
+    d, layers = 4, 4
+    groups = model(d, layers)
+    rng = np.random.default_rng(503)
+    consts = [rng.normal(0, 0.02, (d, d)) for _ in range(layers)]
+    W = [np.repeat(c.reshape(d * d, 1), n // 2, axis=1) for c in consts]
+    s, a, e, ct, sec = secret_inputs(ck, ctx, d, 504)
+    p, got = run(ck, ctx, groups, 1 << 40, [ck.to_device(w) for w in W], sec, ck.to_device(ct))
+    cur = ct.astype(np.uint64)
+    for step, w in zip(p.steps, W):
+        lv = step.level
+        pt = OE.encode_poly(w.reshape(d, d, n // 2), SCALE, qs[:lv], psis[:lv], LOG_N)
+        mac = OL.mac_poly(pt, cur, qs[:lv])
+        cur = OL.rescale(mac, qs[:lv], psis[:lv], LOG_N)
+        if step.refresh_after:
+            cur = OR.refresh(cur, s, a, e, qs, psis, LOG_N, L)
+    assert got.shape == cur.shape
+    assert np.array_equal(got, cur.astype(np.uint32))
