@@ -1,0 +1,76 @@
+"""Baby-step / giant-step diagonal matrix-vector product (CPU oracle; test infrastructure only).
+
+The paper's accelerator linear call is a BSGS matrix-vector product over weight
+diagonals that are encoded once and kept on the device (sections 4.1 and 4.2: the
+BSGS-GEMM objects, 500 to 800 ms per call on its GPU).  The paper does not spell the
+method out; the reading is the Halevi-Shoup diagonal method with the baby-step /
+giant-step split:
+
+* A d x d weight matrix W (d divides the slot count n = N/2) acts on a vector x that
+  is packed d-periodically into the slots: z[t] = x[t mod d].
+* Diagonal k of W, extended d-periodically: diag_k[t] = W[t mod d, (t + k) mod d].
+  Then (W x)[t mod d] = sum_{k < d} diag_k[t] * z[t + k], i.e.
+  W x = sum_k diag_k (.) rot(z, k), where rot(v, r)[t] = v[t + r] (left rotation).
+* With d = n1 * n2 and k = j n1 + i, rot(z, j n1 + i) = rot(rot(z, i), j n1), so
+
+      W x = sum_{j < n2} rot( sum_{i < n1} rot(diag_{j n1 + i}, -j n1) (.) rot(z, i),  j n1 ).
+
+  The plaintexts pt[j, i] = Encode(rot(diag_{j n1 + i}, -j n1)) are the pre-encoded
+  objects; one call takes n1 - 1 baby-step rotations of the input, n2 ct x pt inner
+  sums (the full-polynomial MAC), n2 - 1 giant-step rotations, a sum, and one rescale.
+
+Parity: pinned (tests/test_oracle_keyswitch.py) by decrypting and decoding the result
+against numpy's W @ x, and by the plaintext identity of the diagonal split on random
+matrices.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .keyswitch import rotate
+from .linear import mac_poly, rescale
+
+
+def diagonal_slots(W, n1: int, slots: int) -> np.ndarray:
+    """Slot vectors (n2, n1, slots) of rot(diag_{j n1 + i}, -j n1) for a d x d matrix W."""
+    W = np.asarray(W, dtype=np.float64)
+    d = W.shape[0]
+    if W.shape != (d, d) or slots % d or d % n1:
+        raise ValueError("need a square d x d matrix with d | slots and n1 | d")
+    n2 = d // n1
+    t = np.arange(slots)
+    out = np.empty((n2, n1, slots), dtype=np.float64)
+    for j in range(n2):
+        for i in range(n1):
+            k = j * n1 + i
+            diag = W[t % d, (t + k) % d]
+            out[j, i] = np.roll(diag, j * n1)          # rot(v, -r) = v shifted right by r
+    return out
+
+
+def replicate(x, slots: int) -> np.ndarray:
+    """z[t] = x[t mod d]."""
+    x = np.asarray(x)
+    return x[np.arange(slots) % len(x)]
+
+
+def matvec(pt, ct, n1: int, keys, qs_p, psis_p, log_n: int) -> np.ndarray:
+    """BSGS product of the encoded diagonals pt (n2, n1, L, N) with ct (2, L, N).
+
+    keys: rotation keys by step r (rotation_key(s, r)) for r = 1 .. n1-1 and
+    r = j n1, j = 1 .. n2-1; qs_p / psis_p: the L ciphertext primes and the special
+    prime last.  Returns the rescaled result (2, L-1, N).
+    """
+    pt = np.asarray(pt)
+    n2 = pt.shape[0]
+    L = ct.shape[1]
+    qs = qs_p[:L]
+    baby = [np.asarray(ct, dtype=np.uint64)]
+    for i in range(1, n1):
+        baby.append(rotate(baby[0], i, keys[i], qs_p, psis_p, log_n))
+    inner = mac_poly(pt, np.stack(baby), qs)              # (n2, 2, L, N)
+    q = np.array(qs, dtype=np.uint64)[:, None]
+    acc = inner[0].copy()
+    for j in range(1, n2):
+        acc = (acc + rotate(inner[j], j * n1, keys[j * n1], qs_p, psis_p, log_n)) % q
+    return rescale(acc[None], qs, psis_p[:L], log_n)[0]
