@@ -59,7 +59,8 @@ enum ckks_status {
 enum ckks_op {
   CKKS_OP_MAC_SCALAR = 1, /* a = d_out, b = d_in  */
   CKKS_OP_RESCALE = 2,    /* a = count, b unused  */
-  CKKS_OP_ENCODE_POLY = 3 /* a = count, b unused  */
+  CKKS_OP_ENCODE_POLY = 3, /* a = count, b unused  */
+  CKKS_OP_ROTATE = 4       /* a = count, b = hoisted (0 or 1); limbs = L - 1 */
 };
 
 /* MAC kernel selection for ckks_linear_mac_scalar (ckks_ctx_set_mac_algo). */
@@ -199,6 +200,67 @@ int ckks_decrypt(const ckks_ctx* ctx, const uint32_t* ct, const uint32_t* s_ntt,
 int ckks_refresh(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t limbs_in,
                  const uint32_t* s_ntt, const uint32_t* a, const int32_t* e, uint32_t count,
                  uint32_t limbs_out, uint32_t* ct_out, void* stream);
+
+/* ---- Rotations and the BSGS diagonal matrix-vector product -----------------
+ *
+ * The paper's accelerator linear call is a baby-step / giant-step product of
+ * pre-encoded weight diagonals with rotated copies of the input ciphertext
+ * (sections 4.1 and 4.2), rotations being Galois automorphisms followed by key
+ * switching under one special prime (section 4.2's parameter set).
+ *
+ * Key-switching context: the LAST prime of the context is the special prime P.
+ * Ciphertexts that are rotated, and the BSGS input, carry the other
+ * Lk = L - 1 limbs (L = the context's limb count, at least 3).  Switching keys
+ * are [Lk][2][L][N] words per key (digit i, then the pair (b, a), then every
+ * prime including P), NTT form: ksk_i = (-a_i s + e_i + P g_i s_from, a_i)
+ * with g_i the CRT idempotent of limb i.  Key switching uses one digit per limb
+ * (the centred coefficients of limb i), the digits lifted to every prime,
+ * an inner product with the key and the division by P (the rescale that drops
+ * P).  Rotation by r slots: g = 5^r mod 2N; slot j + r moves to slot j.
+ */
+
+/* sigma_g on NTT-form polynomials: out = the polynomial a(X^g) for each of
+ * `rows` rows of N words (any limb; the permutation does not depend on the
+ * prime).  galois odd, below 2N (5^r mod 2N rotates by r; 2N - 1 conjugates).
+ * in and out must not overlap. */
+int ckks_automorphism(const ckks_ctx* ctx, const uint32_t* in, uint32_t rows, uint32_t galois, uint32_t* out,
+                      void* stream);
+
+/* Rotation keys for steps r0, r0 + r_step, ..., (count keys), under the
+ * secret s_ntt [L][N] (NTT form over every prime of the context, P included).
+ * a: uniform residues [count][Lk][L][N] (NTT form); e: small error
+ * coefficients [count][Lk][N].  ksk: [count][Lk][2][L][N].  Runs on the trusted
+ * side (the secret is an input).  Steps are taken mod N/2. */
+int ckks_keygen_rotation(const ckks_ctx* ctx, const uint32_t* s_ntt, uint32_t r0, uint32_t r_step, uint32_t count,
+                         const uint32_t* a, const int32_t* e, uint32_t* ksk, void* stream);
+
+/* `count` rotations of ciphertexts [..][2][Lk][N]: rotation k is by step
+ * r0 + k r_step with key ksk[k] ([count][Lk][2][L][N]).  hoisted = 1: all count
+ * rotations act on the one ciphertext ct_in (its digits are lifted once);
+ * hoisted = 0: rotation k acts on ct_in[k].  ct_out [count][2][Lk][N] must not
+ * overlap the inputs.  workspace: ckks_workspace_bytes(ctx, CKKS_OP_ROTATE,
+ * count, hoisted, Lk) bytes of device memory, 256-byte aligned. */
+int ckks_rotate(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t count, uint32_t r0, uint32_t r_step,
+                int hoisted, const uint32_t* ksk, void* workspace, size_t workspace_bytes, uint32_t* ct_out,
+                void* stream);
+
+/* BSGS product y = W x of a d x d weight matrix, d = n1 n2, with x packed
+ * d-periodically in the slots of each of `count` input ciphertexts ct_in
+ * [count][2][Lk][N] (Halevi-Shoup diagonals with the baby-step / giant-step
+ * split):  y = sum_j rot( sum_i pt[j][i] (.) rot(x, i), j n1 ), then one rescale.
+ * pt [n2][n1][Lk][N]: NTT-form encodings of rot(diag_(j n1 + i), -j n1) (the
+ * slot vectors diag_k[t] = W[t mod d][(t + k) mod d]; ckks_linear_encode_poly
+ * makes them).  ksk: n1 - 1 rotation keys for steps 1 .. n1-1 followed by
+ * n2 - 1 keys for steps n1, 2 n1, .., (n2-1) n1 ([n1 + n2 - 2][Lk][2][L][N]).
+ * ct_out [count][2][Lk - 1][N] (scale: scale_pt scale_ct / q_(Lk-1)).
+ * workspace: ckks_bsgs_workspace_bytes(ctx, count, n1, n2), 256-byte aligned.
+ * d must divide N/2 (not checked by the library: the caller's packing). */
+int ckks_linear_bsgs(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* ct_in, uint32_t count, uint32_t n1,
+                     uint32_t n2, const uint32_t* ksk, void* workspace, size_t workspace_bytes, uint32_t* ct_out,
+                     void* stream);
+
+/* Workspace of ckks_linear_bsgs in bytes ((size_t)-1 for an invalid request). */
+size_t ckks_bsgs_workspace_bytes(const ckks_ctx* ctx, uint32_t count, uint32_t n1, uint32_t n2);
 
 /* Workspace size in bytes for `op` (ckks_op) with the given sizes; 0 when
  * none is needed; (size_t)-1 for an invalid request. */

@@ -38,6 +38,7 @@ CKKS_E_WORKSPACE = -4
 CKKS_OP_MAC_SCALAR = 1
 CKKS_OP_RESCALE = 2
 CKKS_OP_ENCODE_POLY = 3
+CKKS_OP_ROTATE = 4
 
 CKKS_MAC_AUTO = 0
 CKKS_MAC_VALU = 1
@@ -61,6 +62,11 @@ _SIGS = {
     "ckks_encrypt": (_i32, [_vp, _vp, _vp, _vp, _vp, _u32, _u32, _vp, _vp]),
     "ckks_decrypt": (_i32, [_vp, _vp, _vp, _u32, _u32, _vp, _vp]),
     "ckks_refresh": (_i32, [_vp, _vp, _u32, _vp, _vp, _vp, _u32, _u32, _vp, _vp]),
+    "ckks_automorphism": (_i32, [_vp, _vp, _u32, _u32, _vp, _vp]),
+    "ckks_keygen_rotation": (_i32, [_vp, _vp, _u32, _u32, _u32, _vp, _vp, _vp, _vp]),
+    "ckks_rotate": (_i32, [_vp, _vp, _u32, _u32, _u32, _i32, _vp, _vp, _sz, _vp, _vp]),
+    "ckks_linear_bsgs": (_i32, [_vp, _vp, _vp, _u32, _u32, _u32, _vp, _vp, _sz, _vp, _vp]),
+    "ckks_bsgs_workspace_bytes": (_sz, [_vp, _u32, _u32, _u32]),
     "ckks_workspace_bytes": (_sz, [_vp, _i32, _u32, _u32, _u32]),
     "ckks_rescaled_scale": (_dbl, [_vp, _dbl, _u32]),
     "ckks_last_error": (ctypes.c_char_p, []),
@@ -245,6 +251,60 @@ def ckks_refresh(ctx: Context, ct_in, limbs_in: int, s_ntt, a, e, count: int, li
         _ptr(s_ntt, "s_ntt", max(limbs_out, 2) * n4 if count else 0, 4), _ptr(a, "a", count * limbs_out * n4, 4),
         _ptr(e, "e", count * n4, 4), count, limbs_out, _ptr(ct_out, "ct_out", count * 2 * limbs_out * n4, 4),
         _stream(stream)), "ckks_refresh")
+
+
+def ckks_automorphism(ctx: Context, src, rows: int, galois: int, out, stream=None) -> None:
+    nb = rows * ctx.n * 4
+    _check(_lib.ckks_automorphism(ctx.handle, _ptr(src, "in", nb, 4), rows, galois, _ptr(out, "out", nb, 4),
+                                  _stream(stream)), "ckks_automorphism")
+
+
+def ckks_keygen_rotation(ctx: Context, s_ntt, r0: int, r_step: int, count: int, a, e, ksk, stream=None) -> None:
+    L, n4 = ctx.limbs, ctx.n * 4
+    lk = L - 1
+    _check(_lib.ckks_keygen_rotation(
+        ctx.handle, _ptr(s_ntt, "s_ntt", L * n4 if count else 0, 4), r0 % (ctx.n // 2), r_step % (ctx.n // 2), count,
+        _ptr(a, "a", count * lk * L * n4, 4), _ptr(e, "e", count * lk * n4, 4),
+        _ptr(ksk, "ksk", count * lk * 2 * L * n4, 4), _stream(stream)), "ckks_keygen_rotation")
+
+
+def rotate_workspace_bytes(ctx: Context, count: int, hoisted: bool) -> int:
+    return int(_lib.ckks_workspace_bytes(ctx.handle, CKKS_OP_ROTATE, count, int(hoisted), ctx.limbs - 1))
+
+
+def ckks_rotate(ctx: Context, ct_in, count: int, r0: int, r_step: int, hoisted: bool, ksk, workspace, ct_out,
+                stream=None) -> None:
+    L, n4 = ctx.limbs, ctx.n * 4
+    lk = L - 1
+    wb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.ckks_rotate(
+        ctx.handle, _ptr(ct_in, "ct_in", (1 if hoisted else count) * 2 * lk * n4, 4), count, r0 % (ctx.n // 2),
+        r_step % (ctx.n // 2), int(hoisted), _ptr(ksk, "ksk", count * lk * 2 * L * n4, 4),
+        _ptr(workspace, "workspace", 0, workspace.element_size() if workspace is not None else 1, allow_none=True),
+        wb, _ptr(ct_out, "ct_out", count * 2 * lk * n4, 4), _stream(stream)), "ckks_rotate")
+
+
+def bsgs_workspace_bytes(ctx: Context, count: int, n1: int, n2: int) -> int:
+    return int(_lib.ckks_bsgs_workspace_bytes(ctx.handle, count, n1, n2))
+
+
+def ckks_linear_bsgs(ctx: Context, pt, ct_in, count: int, n1: int, n2: int, ksk, workspace, ct_out,
+                     stream=None) -> None:
+    L, n4 = ctx.limbs, ctx.n * 4
+    lk = L - 1
+    wb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    keys = n1 + n2 - 2
+    _check(_lib.ckks_linear_bsgs(
+        ctx.handle, _ptr(pt, "pt", n1 * n2 * lk * n4, 4), _ptr(ct_in, "ct_in", count * 2 * lk * n4, 4), count, n1, n2,
+        _ptr(ksk, "ksk", keys * lk * 2 * L * n4, 4, allow_none=keys == 0),
+        _ptr(workspace, "workspace", 0, workspace.element_size() if workspace is not None else 1, allow_none=True),
+        wb, _ptr(ct_out, "ct_out", count * 2 * (lk - 1) * n4, 4), _stream(stream)), "ckks_linear_bsgs")
+
+
+def empty_workspace(nbytes: int, device: int = 0):
+    """Device workspace of at least nbytes (torch's allocations are 256-byte aligned)."""
+    import torch
+    return torch.empty((max(nbytes, 1) + 3) // 4, dtype=torch.int32, device=f"cuda:{device}")
 
 
 def ckks_rescaled_scale(ctx: Context, scale_in: float, limbs: int) -> float:

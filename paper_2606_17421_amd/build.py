@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libckkslinear.so")
 
-SOURCES = ["api.cpp", "ntt.hip", "encode.hip", "mac_valu.hip", "mac_mfma.hip", "rescale.hip", "rlwe.hip"]
+SOURCES = ["api.cpp", "ntt.hip", "encode.hip", "mac_valu.hip", "mac_mfma.hip", "rescale.hip", "rlwe.hip", "keyswitch.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -615,6 +615,110 @@ int ckks_refresh(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t limbs_in, 
   return he == hipSuccess ? ok() : hip_fail(he, "refresh launch");
 }
 
+// ---- rotations and the BSGS product ----------------------------------------
+
+static int check_ks_ctx(const ckks_ctx* ctx) {
+  if (int rc = check_ctx(ctx)) return rc;
+  if (ctx->L < 3) return fail(CKKS_E_INVALID_ARG, "key switching needs a context of at least 3 primes (got %u)", ctx->L);
+  return CKKS_OK;
+}
+
+static bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255) == 0; }
+
+int ckks_automorphism(const ckks_ctx* ctx, const uint32_t* in, uint32_t rows, uint32_t galois, uint32_t* out,
+                      void* stream) {
+  if (int rc = check_ctx(ctx)) return rc;
+  if ((galois & 1) == 0 || galois >= 2 * ctx->n) return fail(CKKS_E_INVALID_ARG, "galois=%u not odd below 2N", galois);
+  if (rows == 0) return ok();
+  if (int rc = check_ptr(in, "in")) return rc;
+  if (int rc = check_ptr(out, "out")) return rc;
+  const size_t bytes = size_t(rows) * ctx->n * 4;
+  if (overlaps(in, bytes, out, bytes)) return fail(CKKS_E_INVALID_ARG, "out overlaps in");
+  DeviceGuard guard(ctx->device);
+  hipError_t he = ckks::launch_automorphism(ctx->t, in, rows, galois, out, static_cast<hipStream_t>(stream));
+  return he == hipSuccess ? ok() : hip_fail(he, "automorphism launch");
+}
+
+int ckks_keygen_rotation(const ckks_ctx* ctx, const uint32_t* s_ntt, uint32_t r0, uint32_t r_step, uint32_t count,
+                         const uint32_t* a, const int32_t* e, uint32_t* ksk, void* stream) {
+  if (int rc = check_ks_ctx(ctx)) return rc;
+  if (count == 0) return ok();
+  const size_t L = ctx->L, Lk = L - 1, n = ctx->n;
+  if (int rc = check_rows(ctx, count, static_cast<uint32_t>(Lk * L))) return rc;
+  if (int rc = check_ptr(s_ntt, "s_ntt")) return rc;
+  if (int rc = check_ptr(a, "a")) return rc;
+  if (int rc = check_ptr(e, "e")) return rc;
+  if (int rc = check_ptr(ksk, "ksk")) return rc;
+  const size_t kb = size_t(count) * Lk * 2 * L * n * 4;
+  if (overlaps(ksk, kb, s_ntt, L * n * 4) || overlaps(ksk, kb, a, size_t(count) * Lk * L * n * 4) ||
+      overlaps(ksk, kb, e, size_t(count) * Lk * n * 4))
+    return fail(CKKS_E_INVALID_ARG, "ksk overlaps an input");
+  DeviceGuard guard(ctx->device);
+  hipError_t he = ckks::launch_keygen_rotation(ctx->t, s_ntt, r0, r_step, count, a, e, ksk,
+                                               static_cast<hipStream_t>(stream));
+  return he == hipSuccess ? ok() : hip_fail(he, "keygen_rotation launch");
+}
+
+int ckks_rotate(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t count, uint32_t r0, uint32_t r_step,
+                int hoisted, const uint32_t* ksk, void* workspace, size_t workspace_bytes, uint32_t* ct_out,
+                void* stream) {
+  if (int rc = check_ks_ctx(ctx)) return rc;
+  if (hoisted != 0 && hoisted != 1) return fail(CKKS_E_INVALID_ARG, "hoisted=%d not 0 or 1", hoisted);
+  if (count == 0) return ok();
+  const size_t L = ctx->L, Lk = L - 1, n = ctx->n;
+  if (int rc = check_rows(ctx, count, static_cast<uint32_t>(Lk * L))) return rc;
+  if (int rc = check_ptr(ct_in, "ct_in")) return rc;
+  if (int rc = check_ptr(ksk, "ksk")) return rc;
+  if (int rc = check_ptr(ct_out, "ct_out")) return rc;
+  const size_t need = ckks::rotate_workspace_bytes(ctx->t, hoisted ? 1 : count, count);
+  if (!workspace || workspace_bytes < need)
+    return fail(CKKS_E_WORKSPACE, "rotate workspace %zu bytes < %zu required", workspace_bytes, need);
+  if (!aligned256(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 256-byte aligned");
+  const size_t ctb = 2 * Lk * n * 4, out_b = size_t(count) * ctb;
+  const size_t in_b = (hoisted ? 1 : size_t(count)) * ctb;
+  if (overlaps(ct_out, out_b, ct_in, in_b) || overlaps(ct_out, out_b, ksk, size_t(count) * Lk * 2 * L * n * 4) ||
+      overlaps(workspace, need, ct_in, in_b) || overlaps(workspace, need, ct_out, out_b))
+    return fail(CKKS_E_INVALID_ARG, "ct_out or workspace overlaps another buffer");
+  DeviceGuard guard(ctx->device);
+  hipError_t he = ckks::launch_rotate(ctx->t, ct_in, count, r0, r_step, 0, hoisted == 1, ksk, workspace, ct_out,
+                                      static_cast<hipStream_t>(stream));
+  return he == hipSuccess ? ok() : hip_fail(he, "rotate launch");
+}
+
+size_t ckks_bsgs_workspace_bytes(const ckks_ctx* ctx, uint32_t count, uint32_t n1, uint32_t n2) {
+  if (!ctx || ctx->L < 3 || n1 == 0 || n2 == 0 || n1 > 65536 || n2 > 65536) return static_cast<size_t>(-1);
+  return ckks::bsgs_workspace_bytes(ctx->t, count, n1, n2);
+}
+
+int ckks_linear_bsgs(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* ct_in, uint32_t count, uint32_t n1,
+                     uint32_t n2, const uint32_t* ksk, void* workspace, size_t workspace_bytes, uint32_t* ct_out,
+                     void* stream) {
+  if (int rc = check_ks_ctx(ctx)) return rc;
+  const size_t L = ctx->L, Lk = L - 1, n = ctx->n;
+  if (n1 == 0 || n2 == 0 || size_t(n1) * n2 > n / 2)
+    return fail(CKKS_E_INVALID_ARG, "n1=%u, n2=%u: need n1, n2 >= 1 and n1 n2 <= N/2", n1, n2);
+  if (count == 0) return ok();
+  if (int rc = check_rows(ctx, count, static_cast<uint32_t>(Lk * L * (n1 > n2 ? n1 : n2)))) return rc;
+  if (static_cast<uint64_t>(n2) * Lk * (n / 256) > 0x7FFFFFFFull) return fail(CKKS_E_INVALID_ARG, "n2=%u too large", n2);
+  if (int rc = check_ptr(pt, "pt")) return rc;
+  if (int rc = check_ptr(ct_in, "ct_in")) return rc;
+  if (n1 + n2 > 2 && check_ptr(ksk, "ksk")) return CKKS_E_INVALID_ARG;
+  if (int rc = check_ptr(ct_out, "ct_out")) return rc;
+  const size_t need = ckks::bsgs_workspace_bytes(ctx->t, count, n1, n2);
+  if (!workspace || workspace_bytes < need)
+    return fail(CKKS_E_WORKSPACE, "bsgs workspace %zu bytes < %zu required", workspace_bytes, need);
+  if (!aligned256(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 256-byte aligned");
+  const size_t in_b = size_t(count) * 2 * Lk * n * 4, out_b = size_t(count) * 2 * (Lk - 1) * n * 4;
+  if (overlaps(ct_out, out_b, ct_in, in_b) || overlaps(ct_out, out_b, pt, size_t(n1) * n2 * Lk * n * 4) ||
+      overlaps(workspace, need, ct_in, in_b) || overlaps(workspace, need, ct_out, out_b) ||
+      overlaps(workspace, need, pt, size_t(n1) * n2 * Lk * n * 4))
+    return fail(CKKS_E_INVALID_ARG, "ct_out or workspace overlaps another buffer");
+  DeviceGuard guard(ctx->device);
+  hipError_t he = ckks::launch_bsgs(ctx->t, pt, ct_in, count, n1, n2, ksk, workspace, ct_out,
+                                    static_cast<hipStream_t>(stream));
+  return he == hipSuccess ? ok() : hip_fail(he, "bsgs launch");
+}
+
 size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b, uint32_t limbs) {
   if (!ctx || limbs < 1 || limbs > ctx->L) return static_cast<size_t>(-1);
   switch (op) {
@@ -624,6 +728,9 @@ size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b,
       return limbs < 2 ? static_cast<size_t>(-1) : ckks::rescale_workspace_bytes(ctx->t, a, limbs);
     case CKKS_OP_ENCODE_POLY:
       return 0;
+    case CKKS_OP_ROTATE:
+      if (ctx->L < 3 || limbs != ctx->L - 1 || b > 1) return static_cast<size_t>(-1);
+      return ckks::rotate_workspace_bytes(ctx->t, b ? 1 : a, a);
     default:
       return static_cast<size_t>(-1);
   }

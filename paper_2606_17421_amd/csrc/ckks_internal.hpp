@@ -151,4 +151,19 @@ hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs
                           const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
                           uint32_t* ct_out, hipStream_t s);
 
+// Rotations and the BSGS product (keyswitch.hip).  The context's last prime is
+// the special prime; rotated ciphertexts carry t.L - 1 limbs.
+hipError_t launch_automorphism(const Tables& t, const uint32_t* in, size_t rows, uint32_t galois, uint32_t* out,
+                               hipStream_t s);
+size_t rotate_workspace_bytes(const Tables& t, uint32_t inputs, uint32_t rotations);
+hipError_t launch_rotate(const Tables& t, const uint32_t* ct, uint32_t count, uint32_t r0, uint32_t r_step,
+                         uint32_t galois, bool hoisted, const uint32_t* ksk, void* workspace, uint32_t* out,
+                         hipStream_t s);
+hipError_t launch_keygen_rotation(const Tables& t, const uint32_t* s_ntt, uint32_t r0, uint32_t r_step,
+                                  uint32_t keys, const uint32_t* a, const int32_t* e, uint32_t* ksk,
+                                  hipStream_t s);
+size_t bsgs_workspace_bytes(const Tables& t, uint32_t count, uint32_t n1, uint32_t n2);
+hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, uint32_t count, uint32_t n1,
+                       uint32_t n2, const uint32_t* ksk, void* workspace, uint32_t* out, hipStream_t s);
+
 }  // namespace ckks

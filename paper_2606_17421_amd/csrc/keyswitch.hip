@@ -1,0 +1,429 @@
+// Galois automorphisms, hybrid key switching and slot rotations, and the
+// baby-step / giant-step (BSGS) diagonal matrix-vector product on top of them
+// (gfx950).  The paper's accelerator linear call is a BSGS product over
+// pre-encoded weight diagonals (sections 4.1 and 4.2), with rotations done by
+// automorphisms and key switching under one special prime (section 4.2).
+//
+// Conventions.  The context's last prime P is the special prime; ciphertexts
+// that are rotated carry the other t.L - 1 limbs (L below).  NTT value i is
+// the evaluation at psi^(2 brv(i) + 1), so sigma_g (a(X) -> a(X^g)) permutes
+// NTT values: out[i] = in[brv(u g + (g - 1) / 2 mod N)] with u = brv(i).
+// Rotation by r slots uses g = 5^r mod 2N.
+//
+// Key switching (hybrid, one digit per limb): the digits of c1 are the centred
+// coefficient vectors of its limbs, lifted to every prime of q_0..q_{L-1}, P
+// (ModUp: batched INTT, a lift pass, batched NTT).  A rotation then needs
+// only its key and an index permutation: sigma_g commutes with the digit
+// decomposition exactly (the centred lift is odd-symmetric for odd q), so the
+// inner product reads the unrotated digits through the permutation.  All
+// rotations of one ciphertext share one ModUp (hoisting).  The division by P
+// (ModDown) is the rescale that drops the last prime.
+#include "ntt_core.hpp"
+
+namespace ckks {
+namespace {
+
+constexpr int kThreads = 256;
+
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef int32_t v4s __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ v4u ld4(const uint32_t* p) { return *reinterpret_cast<const v4u*>(p); }
+__device__ __forceinline__ v4s ld4(const int32_t* p) { return *reinterpret_cast<const v4s*>(p); }
+__device__ __forceinline__ void st4(uint32_t* p, v4u v) { *reinterpret_cast<v4u*>(p) = v; }
+
+uint32_t grid_for(size_t threads) { return static_cast<uint32_t>((threads + kThreads - 1) / kThreads); }
+
+// g = 5^r mod 2N (r reduced mod N/2, the order of 5).
+__host__ __device__ __forceinline__ uint32_t galois_of(uint32_t r, uint32_t log_n) {
+  const uint32_t two_n_mask = (2u << log_n) - 1;
+  uint32_t e = r & ((1u << (log_n - 1)) - 1), b = 5, g = 1;
+  while (e) {
+    if (e & 1) g = (g * b) & two_n_mask;
+    b = (b * b) & two_n_mask;
+    e >>= 1;
+  }
+  return g;
+}
+
+// Source index of NTT value i under sigma_g.
+__device__ __forceinline__ uint32_t perm_src(uint32_t i, uint32_t g, uint32_t log_n) {
+  const uint32_t shift = 32 - log_n;
+  const uint32_t u = __builtin_bitreverse32(i) >> shift;
+  const uint32_t v = (u * g + (g >> 1)) & ((1u << log_n) - 1);
+  return __builtin_bitreverse32(v) >> shift;
+}
+
+// A sequence of ciphertexts [2][L][N] in memory: element m sits at ciphertext
+// position (m / grp) * grp_stride + off + m % grp from the base.
+struct Seq {
+  uint32_t grp, grp_stride, off;
+};
+__host__ __device__ __forceinline__ size_t seq_pos(size_t m, Seq q) {
+  return (m / q.grp) * q.grp_stride + q.off + m % q.grp;
+}
+inline Seq contiguous() { return Seq{1, 1, 0}; }
+
+// Rotation k: input m = k / per_input, key slot k % key_period, step
+// r0 + slot * r_step (or the fixed element galois_fixed when nonzero).
+struct RotPlan {
+  uint32_t per_input, key_period, r0, r_step, galois_fixed;
+};
+struct RotIndex {
+  uint32_t m, slot, g;
+};
+__device__ __forceinline__ RotIndex rot_index(uint32_t k, RotPlan p, uint32_t log_n) {
+  RotIndex x;
+  x.m = k / p.per_input;
+  x.slot = k % p.key_period;
+  x.g = p.galois_fixed ? p.galois_fixed : galois_of(p.r0 + x.slot * p.r_step, log_n);
+  return x;
+}
+
+// out[c][p][l][i] = in[c][p][l][perm_g(i)] for rows of N words, one g.
+__global__ __launch_bounds__(kThreads) void automorphism_kernel(Tables tb, const uint32_t* __restrict__ in,
+                                                                size_t rows, uint32_t g,
+                                                                uint32_t* __restrict__ out) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x;
+  const size_t row = i >> tb.log_n;
+  if (row >= rows) return;
+  const uint32_t k = static_cast<uint32_t>(i & (tb.n - 1));
+  out[i] = in[(row << tb.log_n) + perm_src(k, g, tb.log_n)];
+}
+
+// ModUp, step 1: T[m][i] = limb i of c1 of input m (to be inverse-transformed).
+__global__ __launch_bounds__(kThreads) void c1_copy_kernel(Tables tb, const uint32_t* __restrict__ ct, Seq in_seq,
+                                                           uint32_t inputs, uint32_t L, uint32_t* __restrict__ T) {
+  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const size_t per = static_cast<size_t>(L) << tb.log_n;
+  const size_t m = i / per;
+  if (m >= inputs) return;
+  const size_t off = i % per;
+  st4(T + i, ld4(ct + seq_pos(m, in_seq) * 2 * per + per + off));
+}
+
+// ModUp, step 2: D[b][i][j] = centred(T[b][i] mod q_i) mod p_j for every prime
+// j <= L (coefficient form).  Every prime exceeds 2^29 > q_i / 2, so the
+// centred value needs no reduction: v or p_j - (q_i - v).
+__global__ __launch_bounds__(kThreads) void modup_lift_kernel(Tables tb, const uint32_t* __restrict__ T, uint32_t count,
+                                                              uint32_t L, uint32_t* __restrict__ D) {
+  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const size_t rowsz = tb.n;
+  const size_t row = i >> tb.log_n;                        // b * L + digit
+  if (row >= static_cast<size_t>(count) * L) return;
+  const uint32_t digit = static_cast<uint32_t>(row % L);
+  const uint32_t k = static_cast<uint32_t>(i & (tb.n - 1));
+  const uint32_t qi = tb.q[digit], half = qi >> 1;
+  const v4u v = ld4(T + i);
+  uint32_t* dst = D + (row * (L + 1)) * rowsz + k;
+  for (uint32_t j = 0; j <= L; ++j) {
+    const uint32_t pj = tb.q[j];
+    v4u o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = v[e] > half ? pj - (qi - v[e]) : v[e];
+    st4(dst + j * rowsz, o);
+  }
+}
+
+// Key-switch inner product for rotation k (input b, Galois element g):
+//   acc[k][p][j][n] = sum_i D[b][i][j][perm_g(n)] * K[slot][i][p][j][n]   mod p_j,  p in {0, 1}.
+// Products are below 2^60 and at most 15 are summed, so one reduction of the
+// 64-bit sums finishes.
+__global__ __launch_bounds__(kThreads) void ks_inner_kernel(Tables tb, const uint32_t* __restrict__ D,
+                                                            const uint32_t* __restrict__ ksk, uint32_t L,
+                                                            uint32_t rotations, RotPlan plan,
+                                                            uint32_t* __restrict__ acc) {
+  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const uint32_t log_n = tb.log_n, n = tb.n;
+  const size_t row = i >> log_n;                           // k * (L + 1) + j
+  const uint32_t Lp = L + 1;
+  if (row >= static_cast<size_t>(rotations) * Lp) return;
+  const uint32_t k = static_cast<uint32_t>(row / Lp), j = static_cast<uint32_t>(row % Lp);
+  const uint32_t c = static_cast<uint32_t>(i & (n - 1));
+  const RotIndex x = rot_index(k, plan, log_n);
+  uint32_t src[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) src[e] = perm_src(c + e, x.g, log_n);
+  const size_t key_stride = static_cast<size_t>(2) * Lp * n;        // one digit of one key
+  const uint32_t* key = ksk + static_cast<size_t>(x.slot) * L * key_stride + static_cast<size_t>(j) * n + c;
+  const uint32_t* dig = D + (static_cast<size_t>(x.m) * L * Lp + j) * n;
+  uint64_t a0[4] = {0, 0, 0, 0}, a1[4] = {0, 0, 0, 0};
+  for (uint32_t d = 0; d < L; ++d) {
+    const uint32_t* drow = dig + static_cast<size_t>(d) * Lp * n;
+    const v4u k0 = ld4(key + d * key_stride);
+    const v4u k1 = ld4(key + d * key_stride + static_cast<size_t>(Lp) * n);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint64_t dv = drow[src[e]];
+      a0[e] += dv * k0[e];
+      a1[e] += dv * k1[e];
+    }
+  }
+  const uint32_t pj = tb.q[j];
+  const double pr = tb.q_recip[j];
+  v4u o0, o1;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    o0[e] = reduce_u64(a0[e], pj, pr);
+    o1[e] = reduce_u64(a1[e], pj, pr);
+  }
+  uint32_t* out = acc + ((static_cast<size_t>(k) * 2) * Lp + j) * n + c;
+  st4(out, o0);
+  st4(out + static_cast<size_t>(Lp) * n, o1);
+}
+
+// Rotation k's result: out[k] = (sigma_g(c0_m) + u0, u1), u = ModDown(acc[k]) (tmp[k][2][L][N]).
+__global__ __launch_bounds__(kThreads) void rot_combine_kernel(Tables tb, const uint32_t* __restrict__ ct, Seq in_seq,
+                                                               const uint32_t* __restrict__ tmp, uint32_t L,
+                                                               uint32_t rotations, RotPlan plan,
+                                                               uint32_t* __restrict__ out, Seq out_seq) {
+  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const uint32_t log_n = tb.log_n, n = tb.n;
+  const size_t row = i >> log_n;                           // k * L + l
+  if (row >= static_cast<size_t>(rotations) * L) return;
+  const uint32_t k = static_cast<uint32_t>(row / L), l = static_cast<uint32_t>(row % L);
+  const uint32_t c = static_cast<uint32_t>(i & (n - 1));
+  const RotIndex x = rot_index(k, plan, log_n);
+  const size_t ctw = static_cast<size_t>(2) * L * n;
+  const uint32_t* c0 = ct + seq_pos(x.m, in_seq) * ctw + static_cast<size_t>(l) * n;
+  const size_t base = (static_cast<size_t>(k) * 2 * L + l) * n + c;
+  const v4u u0 = ld4(tmp + base);
+  const v4u u1 = ld4(tmp + base + static_cast<size_t>(L) * n);
+  const uint32_t q = tb.q[l];
+  v4u o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = add_mod(c0[perm_src(c + e, x.g, log_n)], u0[e], q);
+  uint32_t* dst = out + seq_pos(k, out_seq) * ctw + static_cast<size_t>(l) * n + c;
+  st4(dst, o);
+  st4(dst + static_cast<size_t>(L) * n, u1);
+}
+
+// Rotation keys, after the error rows have been forward-transformed in the
+// b rows: b_i[j] += -a_i[j] s[j] (+ P s_g[j] when j == i), with s_g = sigma_g(s)
+// read through the permutation of the NTT-form secret.
+__global__ __launch_bounds__(kThreads) void keygen_combine_kernel(Tables tb, const uint32_t* __restrict__ s_ntt,
+                                                                  const uint32_t* __restrict__ a, uint32_t L,
+                                                                  uint32_t keys, uint32_t r0, uint32_t r_step,
+                                                                  uint32_t* __restrict__ ksk) {
+  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const uint32_t log_n = tb.log_n, n = tb.n, Lp = L + 1;
+  const size_t row = i >> log_n;                           // (key * L + digit) * Lp + j
+  if (row >= static_cast<size_t>(keys) * L * Lp) return;
+  const uint32_t j = static_cast<uint32_t>(row % Lp);
+  const size_t kd = row / Lp;                              // key * L + digit
+  const uint32_t digit = static_cast<uint32_t>(kd % L), key = static_cast<uint32_t>(kd / L);
+  const uint32_t c = static_cast<uint32_t>(i & (n - 1));
+  const uint32_t q = tb.q[j], mu = tb.barrett[j];
+  const v4u av = ld4(a + row * n + c);
+  const v4u sv = ld4(s_ntt + static_cast<size_t>(j) * n + c);
+  uint32_t* b = ksk + ((kd * 2) * Lp + j) * n + c;
+  const v4u bv = ld4(b);
+  v4u o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = sub_mod(bv[e], mul_mod_barrett(av[e], sv[e], q, mu), q);
+  if (j == digit) {
+    const uint32_t g = galois_of(r0 + key * r_step, log_n);
+    const uint32_t pm = tb.q[L] % q;                        // P mod q_i
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t sg = s_ntt[static_cast<size_t>(j) * n + perm_src(c + e, g, log_n)];
+      o[e] = add_mod(o[e], mul_mod_barrett(pm, sg, q, mu), q);
+    }
+  }
+  st4(b, o);
+  st4(b + static_cast<size_t>(Lp) * n, av);
+}
+
+// ksk[key][i][0][j] = e[key][i] mod p_j (coefficient form; transformed next).
+__global__ __launch_bounds__(kThreads) void keygen_err_kernel(Tables tb, const int32_t* __restrict__ e, uint32_t L,
+                                                              uint32_t keys, uint32_t* __restrict__ ksk) {
+  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const uint32_t n = tb.n, Lp = L + 1;
+  const size_t row = i >> tb.log_n;                        // key * L + digit
+  if (row >= static_cast<size_t>(keys) * L) return;
+  const uint32_t c = static_cast<uint32_t>(i & (n - 1));
+  const v4s ev = ld4(e + row * n + c);
+  for (uint32_t j = 0; j < Lp; ++j) {
+    const uint32_t q = tb.q[j];
+    v4u r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) r[k] = ev[k] < 0 ? q - static_cast<uint32_t>(-ev[k]) : static_cast<uint32_t>(ev[k]);
+    st4(ksk + ((row * 2) * Lp + j) * n + c, r);
+  }
+}
+
+// out[b][p][l] = sum_j rot[b][j][p][l] (j < terms), the giant-step sum.
+__global__ __launch_bounds__(kThreads) void sum_terms_kernel(Tables tb, const uint32_t* __restrict__ first,
+                                                             size_t first_stride, const uint32_t* __restrict__ rest,
+                                                             uint32_t terms_rest, uint32_t L, uint32_t count,
+                                                             uint32_t* __restrict__ out) {
+  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const size_t per = static_cast<size_t>(2) * L * tb.n;
+  const size_t b = i / per;
+  if (b >= count) return;
+  const size_t off = i % per;
+  const uint32_t l = static_cast<uint32_t>((off >> tb.log_n) % L);
+  const uint32_t q = tb.q[l];
+  v4u s = ld4(first + b * first_stride + off);
+  for (uint32_t j = 0; j < terms_rest; ++j) {
+    const v4u v = ld4(rest + (b * terms_rest + j) * per + off);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s[e] = add_mod(s[e], v[e], q);
+  }
+  st4(out + i, s);
+}
+
+// Workspace of rotate(): T [inputs][L][N], D [inputs][L][L+1][N],
+// acc [rotations][2][L+1][N], tmp [rotations][2][L][N], rescale scratch.
+struct RotWs {
+  uint32_t *T, *D, *acc, *tmp;
+  void* rs;
+  size_t bytes;
+};
+
+RotWs rot_layout(const Tables& t, uint32_t inputs, uint32_t rotations, void* base) {
+  const size_t n = t.n, L = t.L - 1;
+  RotWs w;
+  uint8_t* p = static_cast<uint8_t*>(base);
+  size_t off = 0;
+  auto take = [&](size_t words) {
+    uint8_t* q = p ? p + off : nullptr;
+    off += ((words * 4 + 255) / 256) * 256;
+    return reinterpret_cast<uint32_t*>(q);
+  };
+  w.T = take(inputs * L * n);
+  w.D = take(inputs * L * (L + 1) * n);
+  w.acc = take(rotations * 2 * (L + 1) * n);
+  w.tmp = take(rotations * 2 * L * n);
+  const size_t rs = rescale_workspace_bytes(t, rotations, static_cast<uint32_t>(L + 1));
+  w.rs = p ? p + off : nullptr;
+  off += ((rs + 255) / 256) * 256;
+  w.bytes = off;
+  return w;
+}
+
+}  // namespace
+
+size_t rotate_workspace_bytes(const Tables& t, uint32_t inputs, uint32_t rotations) {
+  return rot_layout(t, inputs, rotations, nullptr).bytes;
+}
+
+hipError_t launch_automorphism(const Tables& t, const uint32_t* in, size_t rows, uint32_t galois, uint32_t* out,
+                               hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  automorphism_kernel<<<grid_for(rows << t.log_n), kThreads, 0, s>>>(t, in, rows, galois, out);
+  return hipGetLastError();
+}
+
+// `rotations` rotations of `inputs` ciphertexts (element m of in_seq from ct):
+// rotation k acts on input k / plan.per_input with key ksk[k % key_period]
+// ([key_period][L][2][L+1][N]) and is written as element k of out_seq.  Each
+// input is decomposed once (ModUp), however many rotations read it.
+hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, uint32_t inputs, uint32_t rotations,
+                             RotPlan plan, const uint32_t* ksk, void* workspace, uint32_t* out, Seq out_seq,
+                             hipStream_t s) {
+  if (rotations == 0) return hipSuccess;
+  const uint32_t L = t.L - 1, Lp = L + 1;
+  const size_t n = t.n;
+  RotWs w = rot_layout(t, inputs, rotations, workspace);
+  c1_copy_kernel<<<grid_for(inputs * L * n / 4), kThreads, 0, s>>>(t, ct, in_seq, inputs, L, w.T);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  err = launch_ntt(t, w.T, static_cast<size_t>(inputs) * L, L, true, s);
+  if (err != hipSuccess) return err;
+  modup_lift_kernel<<<grid_for(inputs * L * n / 4), kThreads, 0, s>>>(t, w.T, inputs, L, w.D);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  err = launch_ntt(t, w.D, static_cast<size_t>(inputs) * L * Lp, Lp, false, s);
+  if (err != hipSuccess) return err;
+  ks_inner_kernel<<<grid_for(static_cast<size_t>(rotations) * Lp * n / 4), kThreads, 0, s>>>(t, w.D, ksk, L,
+                                                                                            rotations, plan, w.acc);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  err = launch_rescale(t, w.acc, w.tmp, rotations, Lp, w.rs, s);
+  if (err != hipSuccess) return err;
+  rot_combine_kernel<<<grid_for(static_cast<size_t>(rotations) * L * n / 4), kThreads, 0, s>>>(
+      t, ct, in_seq, w.tmp, L, rotations, plan, out, out_seq);
+  return hipGetLastError();
+}
+
+hipError_t launch_keygen_rotation(const Tables& t, const uint32_t* s_ntt, uint32_t r0, uint32_t r_step,
+                                  uint32_t keys, const uint32_t* a, const int32_t* e, uint32_t* ksk,
+                                  hipStream_t s) {
+  if (keys == 0) return hipSuccess;
+  const uint32_t L = t.L - 1, Lp = L + 1;
+  const size_t n = t.n;
+  keygen_err_kernel<<<grid_for(static_cast<size_t>(keys) * L * n / 4), kThreads, 0, s>>>(t, e, L, keys, ksk);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  // the b rows: logical row (key * L + digit) * Lp + j is physical row (.. / Lp) * 2 Lp + j
+  err = launch_ntt(t, ksk, static_cast<size_t>(keys) * L * Lp, Lp, false, s, 2 * Lp);
+  if (err != hipSuccess) return err;
+  keygen_combine_kernel<<<grid_for(static_cast<size_t>(keys) * L * Lp * n / 4), kThreads, 0, s>>>(
+      t, s_ntt, a, L, keys, r0, r_step, ksk);
+  return hipGetLastError();
+}
+
+// Workspace of the BSGS product for `count` input ciphertexts: baby rotations
+// [count][n1][2][L][N], inner sums [count][n2][2][L][N], giant rotations
+// [count][n2-1][2][L][N], the sum [count][2][L][N], and the largest of the two
+// rotation workspaces and the closing rescale's.
+size_t bsgs_workspace_bytes(const Tables& t, uint32_t count, uint32_t n1, uint32_t n2) {
+  const size_t ct = static_cast<size_t>(2) * (t.L - 1) * t.n * 4;
+  const size_t fixed = ct * count * (static_cast<size_t>(n1) + n2 + (n2 - 1) + 1);
+  size_t scratch = rotate_workspace_bytes(t, count, count * (n1 - 1));
+  const size_t rot2 = rotate_workspace_bytes(t, count * (n2 - 1), count * (n2 - 1));
+  const size_t rs = rescale_workspace_bytes(t, count, t.L - 1);   // the closing rescale
+  scratch = scratch > rot2 ? scratch : rot2;
+  return fixed + (scratch > rs ? scratch : rs);
+}
+
+hipError_t launch_rotate(const Tables& t, const uint32_t* ct, uint32_t count, uint32_t r0, uint32_t r_step,
+                         uint32_t galois, bool hoisted, const uint32_t* ksk, void* workspace, uint32_t* out,
+                         hipStream_t s) {
+  // hoisted: count rotations of one input; else rotation k of input k
+  RotPlan plan{hoisted ? count : 1u, count, r0, r_step, galois};
+  return launch_rotate_seq(t, ct, contiguous(), hoisted ? 1 : count, count, plan, ksk, workspace, out, contiguous(),
+                           s);
+}
+
+// y = sum_j rot( sum_i pt[j][i] (.) rot(x, i), j n1 ), rescaled, for each of
+// `count` inputs.  pt [n2][n1][L][N]; ksk: n1 - 1 baby keys (steps 1 .. n1-1)
+// then n2 - 1 giant keys (steps n1, 2 n1, ..); out [count][2][L-1][N].
+hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, uint32_t count, uint32_t n1,
+                       uint32_t n2, const uint32_t* ksk, void* workspace, uint32_t* out, hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  const uint32_t L = t.L - 1;
+  const size_t n = t.n, ctw = 2 * L * n;
+  const size_t key_words = static_cast<size_t>(L) * 2 * (L + 1) * n;
+  uint32_t* baby = static_cast<uint32_t*>(workspace);
+  uint32_t* inner = baby + static_cast<size_t>(count) * n1 * ctw;
+  uint32_t* giant = inner + static_cast<size_t>(count) * n2 * ctw;
+  uint32_t* sum = giant + static_cast<size_t>(count) * (n2 - 1) * ctw;
+  void* rws = sum + static_cast<size_t>(count) * ctw;
+  // baby steps: element 0 of each input's group is the input itself, then its
+  // rotations by 1 .. n1-1 (one ModUp per input)
+  hipError_t err = hipMemcpy2DAsync(baby, n1 * ctw * 4, ct, ctw * 4, ctw * 4, count, hipMemcpyDeviceToDevice, s);
+  if (err != hipSuccess) return err;
+  if (n1 > 1) {
+    RotPlan plan{n1 - 1, n1 - 1, 1, 1, 0};
+    err = launch_rotate_seq(t, ct, contiguous(), count, count * (n1 - 1), plan, ksk, rws, baby,
+                            Seq{n1 - 1, n1, 1}, s);
+    if (err != hipSuccess) return err;
+  }
+  // inner sums: one full-polynomial MAC per input
+  for (uint32_t b = 0; b < count; ++b) {
+    err = launch_mac_poly(t, pt, baby + static_cast<size_t>(b) * n1 * ctw, inner + static_cast<size_t>(b) * n2 * ctw,
+                          n2, n1, L, s);
+    if (err != hipSuccess) return err;
+  }
+  // giant steps: inner sum j >= 1 of every input rotated by j n1
+  if (n2 > 1) {
+    RotPlan plan{1, n2 - 1, n1, n1, 0};
+    err = launch_rotate_seq(t, inner, Seq{n2 - 1, n2, 1}, count * (n2 - 1), count * (n2 - 1), plan,
+                            ksk + static_cast<size_t>(n1 - 1) * key_words, rws, giant, contiguous(), s);
+    if (err != hipSuccess) return err;
+  }
+  sum_terms_kernel<<<grid_for(count * ctw / 4), kThreads, 0, s>>>(t, inner, n2 * ctw, giant, n2 - 1, L, count, sum);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  return launch_rescale(t, sum, out, count, L, rws, s);
+}
+
+}  // namespace ckks

@@ -1,0 +1,179 @@
+"""GPU parity of the automorphism, rotation-key generation, rotation (hoisted
+and per-input) and BSGS entry points against the oracle, bit for bit, and the
+BSGS product end to end against numpy's W @ x.
+
+The context holds the ciphertext primes and the special prime last; every
+expected value is computed by the oracle from host-side integers."""
+import numpy as np
+import pytest
+
+from oracle import bsgs as OB
+from oracle import encode as OE
+from oracle import keyswitch as KS
+from oracle import rlwe as OR
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+_CTX = {}
+
+
+def ctx_for(ck, log_n, L):
+    """Context with L ciphertext primes and the special prime (L + 1 primes)."""
+    key = (log_n, L)
+    if key not in _CTX:
+        _CTX[key] = ck.Context(log_n, L + 1)
+    return _CTX[key]
+
+
+def setup(ck, log_n, L, seed):
+    ctx = ctx_for(ck, log_n, L)
+    qs_p, psis_p, n = list(ctx.moduli), list(ctx.roots), ctx.n
+    st = gen.streams(seed, log_n)
+    s = gen.ternary_secret(st["secret"], n)
+    s_ntt = ck.to_device(np.stack([np.mod(s, q) for q in qs_p]).astype(np.uint32))
+    ck.ckks_ntt(ctx, s_ntt, 1, L + 1)
+    return ctx, qs_p, psis_p, n, st, s, s_ntt
+
+
+def oracle_keys(st, s, steps, qs_p, psis_p, log_n):
+    L, n = len(qs_p) - 1, 1 << log_n
+    out = []
+    for r in steps:
+        a = gen.uniform_residues(st["residues"], (L,), qs_p, n)
+        e = gen.gaussian_error(st["error"], (L, n))
+        out.append(KS.rotation_key(s, r, a, e, qs_p, psis_p, log_n))
+    return np.stack(out).astype(np.uint32)                        # (keys, L, 2, L+1, N)
+
+
+@pytest.mark.parametrize("log_n", [10, 13, 16])
+def test_automorphism_bit_exact(gpu_lib, log_n):
+    ck = gpu_lib
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, 2, 700 + log_n)
+    rows = gen.uniform_residues(st["residues"], (2,), qs_p, n)           # (2, 3, N): row r uses prime r % 3
+    d_in = ck.to_device(rows)
+    d_out = ck.empty_u32(rows.shape)
+    for g in (KS.galois_element(1, log_n), KS.galois_element(77, log_n), 2 * n - 1):
+        ck.ckks_automorphism(ctx, d_in, 6, g, d_out)
+        got = ck.to_host_u32(d_out)
+        for c in range(2):
+            for l in range(3):
+                want = KS.automorphism_ntt(rows[c, l], g, qs_p[l], psis_p[l], log_n)
+                assert np.array_equal(got[c, l], want.astype(np.uint32)), (g, c, l)
+
+
+@pytest.mark.parametrize("log_n,L,r0,r_step,count", [(10, 2, 1, 1, 3), (13, 4, 8, 8, 2)])
+def test_keygen_rotation_bit_exact(gpu_lib, log_n, L, r0, r_step, count):
+    ck = gpu_lib
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 720 + log_n)
+    a = gen.uniform_residues(st["residues"], (count, L), qs_p, n)         # (count, L, L+1, N)
+    e = gen.gaussian_error(st["error"], (count, L, n)).astype(np.int32)
+    ksk = ck.empty_u32((count, L, 2, L + 1, n))
+    ck.ckks_keygen_rotation(ctx, s_ntt, r0, r_step, count, ck.to_device(a), ck.to_device(e), ksk)
+    got = ck.to_host_u32(ksk)
+    for k in range(count):
+        want = KS.rotation_key(s, r0 + k * r_step, a[k], e[k], qs_p, psis_p, log_n)
+        assert np.array_equal(got[k], want.astype(np.uint32)), k
+
+
+@pytest.mark.parametrize("log_n,L,hoisted,steps", [(10, 2, True, (1, 2, 3)), (10, 3, False, (5, 9)),
+                                                   (12, 3, True, (4, 8)), (16, 2, False, (1,))])
+def test_rotate_bit_exact(gpu_lib, log_n, L, hoisted, steps):
+    ck = gpu_lib
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 740 + log_n + L)
+    count = len(steps)
+    r0, r_step = steps[0], (steps[1] - steps[0]) if count > 1 else 1
+    assert list(steps) == [r0 + k * r_step for k in range(count)]
+    cts = gen.uniform_residues(st["residues"], (1 if hoisted else count, 2), qs_p[:L], n)
+    keys = oracle_keys(st, s, steps, qs_p, psis_p, log_n)
+    ws = ck.empty_workspace(ck.rotate_workspace_bytes(ctx, count, hoisted))
+    out = ck.empty_u32((count, 2, L, n))
+    ck.ckks_rotate(ctx, ck.to_device(cts), count, r0, r_step, hoisted, ck.to_device(keys), ws, out)
+    got = ck.to_host_u32(out)
+    for k, r in enumerate(steps):
+        src = cts[0] if hoisted else cts[k]
+        want = KS.rotate(src.astype(np.uint64), r, keys[k], qs_p, psis_p, log_n)
+        assert np.array_equal(got[k], want.astype(np.uint32)), (k, r)
+
+
+@pytest.mark.parametrize("log_n,L,n1,n2,count", [(10, 2, 4, 4, 2), (11, 3, 3, 5, 1), (10, 3, 1, 4, 1),
+                                                 (10, 2, 4, 1, 1)])
+def test_bsgs_bit_exact(gpu_lib, log_n, L, n1, n2, count):
+    """Any residues: the product is exact modular arithmetic, so uniform plaintexts and
+    ciphertexts are compared with the oracle bit for bit."""
+    ck = gpu_lib
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 760 + n1 * 7 + n2)
+    pt = gen.uniform_residues(st["residues"], (n2, n1), qs_p[:L], n)
+    cts = gen.uniform_residues(st["residues"], (count, 2), qs_p[:L], n)
+    steps = list(range(1, n1)) + [j * n1 for j in range(1, n2)]
+    keys = oracle_keys(st, s, steps, qs_p, psis_p, log_n) if steps else None
+    ws = ck.empty_workspace(ck.bsgs_workspace_bytes(ctx, count, n1, n2))
+    out = ck.empty_u32((count, 2, L - 1, n))
+    ck.ckks_linear_bsgs(ctx, ck.to_device(pt), ck.to_device(cts), count, n1, n2,
+                        ck.to_device(keys) if keys is not None else None, ws, out)
+    got = ck.to_host_u32(out)
+    kd = {r: keys[i] for i, r in enumerate(steps)}
+    for b in range(count):
+        want = OB.matvec(pt, cts[b].astype(np.uint64), n1, kd, qs_p, psis_p, log_n)
+        assert np.array_equal(got[b], want.astype(np.uint32)), b
+
+
+def test_bsgs_end_to_end_matches_w_times_x(gpu_lib):
+    """Diagonals encoded and keys generated on the GPU; the decrypted, decoded
+    product equals numpy's W @ x for every slot (d = 64, N = 2^12)."""
+    ck = gpu_lib
+    log_n, L, d, n1 = 12, 3, 64, 8
+    n2 = d // n1
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 781)
+    qs, psis, slots = qs_p[:L], psis_p[:L], n // 2
+    delta = float(2 ** 26)
+    W = st["weights"].normal(0, 0.1, (d, d))
+    x = st["activations"].normal(0, 1, d)
+    diag = OB.diagonal_slots(W, n1, slots).reshape(n2 * n1, slots)
+    pt = ck.empty_u32((n2, n1, L, n))
+    ck.ckks_linear_encode_poly(ctx, ck.to_device(diag), n2 * n1, L, delta, pt)
+    m = OE.round_coeffs(OE.encode_coeffs(OB.replicate(x, slots), log_n), delta)
+    ct = OR.encrypt(m, s, gen.uniform_residues(st["residues"], (), qs, n), gen.gaussian_error(st["error"], n),
+                    qs, psis, log_n).astype(np.uint32)
+    steps_b, steps_g = n1 - 1, n2 - 1
+    a = gen.uniform_residues(st["residues"], (steps_b + steps_g, L), qs_p, n)
+    e = gen.gaussian_error(st["error"], (steps_b + steps_g, L, n)).astype(np.int32)
+    ksk = ck.empty_u32((steps_b + steps_g, L, 2, L + 1, n))
+    key_words = L * 2 * (L + 1) * n
+    flat = ksk.view(-1)
+    ck.ckks_keygen_rotation(ctx, s_ntt, 1, 1, steps_b, ck.to_device(a[:steps_b]), ck.to_device(e[:steps_b]),
+                            flat[: steps_b * key_words])
+    ck.ckks_keygen_rotation(ctx, s_ntt, n1, n1, steps_g, ck.to_device(a[steps_b:]), ck.to_device(e[steps_b:]),
+                            flat[steps_b * key_words:])
+    ws = ck.empty_workspace(ck.bsgs_workspace_bytes(ctx, 1, n1, n2))
+    out = ck.empty_u32((1, 2, L - 1, n))
+    ck.ckks_linear_bsgs(ctx, pt, ck.to_device(ct[None]), 1, n1, n2, ksk, ws, out)
+    res = ck.to_host_u32(out)[0].astype(np.uint64)
+    dec = np.array(OR.decrypt(res, s, qs[:L - 1], psis[:L - 1], log_n), dtype=np.float64)
+    y = OE.decode(dec, delta * delta / qs[L - 1], log_n).real
+    assert np.max(np.abs(y - OB.replicate(W @ x, slots))) < 1e-3
+
+
+def test_rotation_argument_errors(gpu_lib):
+    ck = gpu_lib
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, 10, 2, 790)
+    ct = ck.empty_u32((1, 2, 2, n))
+    out = ck.empty_u32((2, 2, 2, n))
+    ksk = ck.empty_u32((2, 2, 2, 3, n))
+    small = ck.empty_workspace(64)
+    with pytest.raises(ck.CkksError) as ex:
+        ck.ckks_rotate(ctx, ct, 2, 1, 1, True, ksk, small, out)
+    assert ex.value.code == ck.CKKS_E_WORKSPACE
+    with pytest.raises(ck.CkksError) as ex:
+        ck.ckks_automorphism(ctx, ct, 4, 6, out)                       # even element
+    assert ex.value.code == ck.CKKS_E_INVALID_ARG
+    import ctypes
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+    ws = ck.empty_workspace(1 << 20)
+    rc = ck._lib.ckks_linear_bsgs(ctx.handle, P(ksk), P(ct), 1, 32, 32, P(ksk), P(ws), 1 << 20, P(out), None)
+    assert rc == ck.CKKS_E_INVALID_ARG and "n1 n2 <= N/2" in ck.ckks_last_error()   # d = 1024 > N/2
+    two = ck.Context(10, 2)
+    with pytest.raises(ck.CkksError) as ex:                              # no room for the special prime
+        ck.ckks_rotate(two, ck.empty_u32((1, 2, 1, n)), 1, 1, 1, True, ck.empty_u32((1, 1, 2, 2, n)), small,
+                       ck.empty_u32((1, 2, 1, n)))
+    assert ex.value.code == ck.CKKS_E_INVALID_ARG
