@@ -8,14 +8,19 @@
 // residues stay in registers (group-0 layout, which is also the forward
 // transform's starting layout) while each remaining limb is forward-
 // transformed and combined with c_l on the way out.  HBM traffic is the
-// minimum: read limbs rows, write limbs - 1 rows.
+// minimum: read limbs rows, write limbs - 1 rows.  When the polynomials are
+// fewer than half the CUs (the key-switch ModDown of a few rotations, a
+// decode-size layer), each workgroup instead takes one output limb of one
+// polynomial (kSplit): the inverse transform is repeated per limb, but the
+// chain per workgroup is two transforms instead of limbs, on limbs - 1 times
+// the workgroups.
 // N = 2^16: three passes through a workspace (see below).
 #include "ntt_core.hpp"
 
 namespace ckks {
 namespace {
 
-template <int LOGN>
+template <int LOGN, bool kSplit>
 __global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSimd) void rescale_kernel(
     Tables tb, const uint32_t* __restrict__ in, uint32_t* __restrict__ out, uint32_t limbs) {
   using P = typename WholePlan<LOGN>::P;
@@ -53,7 +58,8 @@ __global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSi
     r[j] = x > (qt >> 1) ? static_cast<int32_t>(x) - static_cast<int32_t>(qt) : static_cast<int32_t>(x);
   }
 
-  for (uint32_t l = 0; l < top; ++l) {
+  const uint32_t l_begin = kSplit ? blockIdx.y : 0, l_end = kSplit ? blockIdx.y + 1 : top;
+  for (uint32_t l = l_begin; l < l_end; ++l) {
     const uint32_t q = tb.q[l];
 #pragma unroll
     for (int j = 0; j < P::E; ++j) v[j] = static_cast<uint32_t>(r[j] < 0 ? r[j] + static_cast<int32_t>(q) : r[j]);
@@ -208,7 +214,10 @@ hipError_t rescale16(const Tables& t, const uint32_t* in, uint32_t* out, uint32_
 template <int LOGN>
 hipError_t launch_rescale_whole(const Tables& t, const uint32_t* in, uint32_t* out, uint32_t count,
                                 uint32_t limbs, hipStream_t s) {
-  rescale_kernel<LOGN><<<dim3(2 * count), WholePlan<LOGN>::P::T, 0, s>>>(t, in, out, limbs);
+  if (4 * static_cast<size_t>(count) <= t.num_cus && limbs > 2)
+    rescale_kernel<LOGN, true><<<dim3(2 * count, limbs - 1), WholePlan<LOGN>::P::T, 0, s>>>(t, in, out, limbs);
+  else
+    rescale_kernel<LOGN, false><<<dim3(2 * count), WholePlan<LOGN>::P::T, 0, s>>>(t, in, out, limbs);
   return hipGetLastError();
 }
 

@@ -172,7 +172,11 @@ __global__ __launch_bounds__(kThreads) void dte_lift_kernel(Tables tb, const int
 // + limbs_out (error, L2) in, 2 limbs_out out; the multi-pass route moves
 // 13 + 7 limbs_out.
 // 16 residues per thread up to 2^14 (1024 threads) keeps the live state in
-// registers.
+// registers.  With fewer ciphertexts than half the CUs (a decode-size group)
+// each workgroup takes one output limb of one ciphertext (kSplit): the two
+// inverse transforms are repeated per limb, but the chain per workgroup is
+// three transforms instead of 2 + limbs_out, on limbs_out times the
+// workgroups.
 template <int LOGN>
 struct RefreshPlan {
   static_assert(LOGN <= 14, "the fused refresh serves N <= 2^14");
@@ -181,7 +185,7 @@ struct RefreshPlan {
   static constexpr int kWavesPerSimd = 4;
 };
 
-template <int LOGN>
+template <int LOGN, bool kSplit>
 __global__ __launch_bounds__(RefreshPlan<LOGN>::P::T, RefreshPlan<LOGN>::kWavesPerSimd) void refresh_kernel(
     Tables tb, const uint32_t* __restrict__ ct_in, uint32_t limbs_in, const uint32_t* __restrict__ s_ntt,
     const uint32_t* __restrict__ a, const int32_t* __restrict__ e, uint32_t limbs_out,
@@ -234,7 +238,8 @@ __global__ __launch_bounds__(RefreshPlan<LOGN>::P::T, RefreshPlan<LOGN>::kWavesP
   }
   // the error row through a buffer resource: the per-j offsets j T are scalar constants
   const auto er = row_rsrc(e + c * N, N);
-  for (uint32_t l = 0; l < limbs_out; ++l) {
+  const uint32_t l_begin = kSplit ? blockIdx.y : 0, l_end = kSplit ? blockIdx.y + 1 : limbs_out;
+  for (uint32_t l = l_begin; l < l_end; ++l) {
     const uint32_t q = tb.q[l], mu = tb.barrett[l];
     const uint32_t q0l = q0 >= q ? q0 - q : q0, q1l = q1 >= q ? q1 - q : q1;  // q0, q1 < 2q
     const uint32_t q2l = mul_mod_barrett(q0l, q1l, q, mu);                      // q0 q1 mod q
@@ -268,7 +273,12 @@ template <int LOGN>
 hipError_t launch_refresh_fused(const Tables& t, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
                                 const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
                                 uint32_t* ct_out, hipStream_t s) {
-  refresh_kernel<LOGN><<<count, RefreshPlan<LOGN>::P::T, 0, s>>>(t, ct_in, limbs_in, s_ntt, a, e, limbs_out, ct_out);
+  if (2 * static_cast<size_t>(count) <= t.num_cus && limbs_out > 1)
+    refresh_kernel<LOGN, true><<<dim3(count, limbs_out), RefreshPlan<LOGN>::P::T, 0, s>>>(t, ct_in, limbs_in, s_ntt, a,
+                                                                                        e, limbs_out, ct_out);
+  else
+    refresh_kernel<LOGN, false><<<dim3(count), RefreshPlan<LOGN>::P::T, 0, s>>>(t, ct_in, limbs_in, s_ntt, a, e,
+                                                                               limbs_out, ct_out);
   return hipGetLastError();
 }
 

@@ -137,7 +137,7 @@ def test_mac_poly_bit_exact(gpu_lib, log_n, limbs, d_in, d_out):
 
 
 @pytest.mark.parametrize("log_n,limbs,count", [(10, 2, 3), (11, 3, 2), (12, 4, 1), (13, 2, 1), (14, 3, 1),
-                                               (15, 2, 1), (16, 3, 1)])
+                                               (15, 2, 1), (16, 3, 1), (10, 4, 70), (12, 3, 65)])
 def test_rescale_bit_exact(gpu_lib, log_n, limbs, count):
     ck = gpu_lib
     ctx = ctx_for(ck, log_n, max(limbs, 3))
