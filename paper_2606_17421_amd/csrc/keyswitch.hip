@@ -124,51 +124,57 @@ __global__ __launch_bounds__(kThreads) void modup_lift_kernel(Tables tb, const u
   }
 }
 
-// Key-switch inner product for rotation k (input b, Galois element g):
-//   acc[k][p][j][n] = sum_i D[b][i][j][perm_g(n)] * K[slot][i][p][j][n]   mod p_j,  p in {0, 1}.
+// Key-switch inner product for rotation k (input m, Galois element g):
+//   acc[k][p][j][n] = sum_i D[m][i][j][perm_g(n)] * K[slot][i][p][j][n]   mod p_j,  p in {0, 1}.
 // Products are below 2^60 and at most 15 are summed, so one reduction of the
-// 64-bit sums finishes.
+// 64-bit sums finishes.  A thread serves one key slot and loops over the
+// rotations that use that key (k = u * key_period + slot, one per input of a
+// batch), so each key is streamed from HBM once per call and re-read from
+// cache by the same thread.
 __global__ __launch_bounds__(kThreads) void ks_inner_kernel(Tables tb, const uint32_t* __restrict__ D,
                                                             const uint32_t* __restrict__ ksk, uint32_t L,
                                                             uint32_t rotations, RotPlan plan,
                                                             uint32_t* __restrict__ acc) {
   const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
   const uint32_t log_n = tb.log_n, n = tb.n;
-  const size_t row = i >> log_n;                           // k * (L + 1) + j
+  const size_t row = i >> log_n;                           // slot * (L + 1) + j
   const uint32_t Lp = L + 1;
-  if (row >= static_cast<size_t>(rotations) * Lp) return;
-  const uint32_t k = static_cast<uint32_t>(row / Lp), j = static_cast<uint32_t>(row % Lp);
+  if (row >= static_cast<size_t>(plan.key_period) * Lp) return;
+  const uint32_t slot = static_cast<uint32_t>(row / Lp), j = static_cast<uint32_t>(row % Lp);
   const uint32_t c = static_cast<uint32_t>(i & (n - 1));
-  const RotIndex x = rot_index(k, plan, log_n);
+  const RotIndex x0 = rot_index(slot, plan, log_n);        // the element depends on the slot only
   uint32_t src[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) src[e] = perm_src(c + e, x.g, log_n);
+  for (int e = 0; e < 4; ++e) src[e] = perm_src(c + e, x0.g, log_n);
   const size_t key_stride = static_cast<size_t>(2) * Lp * n;        // one digit of one key
-  const uint32_t* key = ksk + static_cast<size_t>(x.slot) * L * key_stride + static_cast<size_t>(j) * n + c;
-  const uint32_t* dig = D + (static_cast<size_t>(x.m) * L * Lp + j) * n;
-  uint64_t a0[4] = {0, 0, 0, 0}, a1[4] = {0, 0, 0, 0};
-  for (uint32_t d = 0; d < L; ++d) {
-    const uint32_t* drow = dig + static_cast<size_t>(d) * Lp * n;
-    const v4u k0 = ld4(key + d * key_stride);
-    const v4u k1 = ld4(key + d * key_stride + static_cast<size_t>(Lp) * n);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint64_t dv = drow[src[e]];
-      a0[e] += dv * k0[e];
-      a1[e] += dv * k1[e];
-    }
-  }
+  const uint32_t* key = ksk + static_cast<size_t>(slot) * L * key_stride + static_cast<size_t>(j) * n + c;
   const uint32_t pj = tb.q[j];
   const double pr = tb.q_recip[j];
-  v4u o0, o1;
+  for (uint32_t k = slot; k < rotations; k += plan.key_period) {
+    const uint32_t m = k / plan.per_input;
+    const uint32_t* dig = D + (static_cast<size_t>(m) * L * Lp + j) * n;
+    uint64_t a0[4] = {0, 0, 0, 0}, a1[4] = {0, 0, 0, 0};
+    for (uint32_t d = 0; d < L; ++d) {
+      const uint32_t* drow = dig + static_cast<size_t>(d) * Lp * n;
+      const v4u k0 = ld4(key + d * key_stride);
+      const v4u k1 = ld4(key + d * key_stride + static_cast<size_t>(Lp) * n);
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    o0[e] = reduce_u64(a0[e], pj, pr);
-    o1[e] = reduce_u64(a1[e], pj, pr);
+      for (int e = 0; e < 4; ++e) {
+        const uint64_t dv = drow[src[e]];
+        a0[e] += dv * k0[e];
+        a1[e] += dv * k1[e];
+      }
+    }
+    v4u o0, o1;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o0[e] = reduce_u64(a0[e], pj, pr);
+      o1[e] = reduce_u64(a1[e], pj, pr);
+    }
+    uint32_t* out = acc + ((static_cast<size_t>(k) * 2) * Lp + j) * n + c;
+    st4(out, o0);
+    st4(out + static_cast<size_t>(Lp) * n, o1);
   }
-  uint32_t* out = acc + ((static_cast<size_t>(k) * 2) * Lp + j) * n + c;
-  st4(out, o0);
-  st4(out + static_cast<size_t>(Lp) * n, o1);
 }
 
 // Rotation k's result: out[k] = (sigma_g(c0_m) + u0, u1), u = ModDown(acc[k]) (tmp[k][2][L][N]).
@@ -251,25 +257,109 @@ __global__ __launch_bounds__(kThreads) void keygen_err_kernel(Tables tb, const i
   }
 }
 
-// out[b][p][l] = sum_j rot[b][j][p][l] (j < terms), the giant-step sum.
-__global__ __launch_bounds__(kThreads) void sum_terms_kernel(Tables tb, const uint32_t* __restrict__ first,
-                                                             size_t first_stride, const uint32_t* __restrict__ rest,
-                                                             uint32_t terms_rest, uint32_t L, uint32_t count,
+// Giant-step sum fused with the rotations' final step: for input b,
+//   out[b] = inner[b][0] + sum_{j=1}^{n2-1} ( (sigma_gj(c0 of inner[b][j]), 0) + u[b][j] ),
+// u[b][j] = tmp[b (n2-1) + j - 1] (ModDown outputs), g_j = g1^j with g1 = 5^n1.
+// A workgroup takes 64 consecutive coefficients; its 4 waves sum the terms
+// j = 1 + w, 5 + w, .. (independent loads in flight) and combine through LDS.
+__global__ __launch_bounds__(kThreads) void giant_sum_kernel(Tables tb, const uint32_t* __restrict__ inner,
+                                                             const uint32_t* __restrict__ tmp, uint32_t L,
+                                                             uint32_t count, uint32_t n2, uint32_t g1,
                                                              uint32_t* __restrict__ out) {
-  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
-  const size_t per = static_cast<size_t>(2) * L * tb.n;
-  const size_t b = i / per;
+  __shared__ uint32_t part[3][64];
+  const uint32_t lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const size_t i = static_cast<size_t>(blockIdx.x) * 64 + lane;
+  const uint32_t log_n = tb.log_n, n = tb.n;
+  const size_t ctw = static_cast<size_t>(2) * L * n;
+  const size_t b = i / ctw;                                 // workgroup-uniform (64 | ctw)
   if (b >= count) return;
-  const size_t off = i % per;
-  const uint32_t l = static_cast<uint32_t>((off >> tb.log_n) % L);
+  const size_t off = i % ctw;                               // (p * L + l) * N + c
+  const uint32_t pl = static_cast<uint32_t>(off >> log_n);
+  const uint32_t l = pl % L, c = static_cast<uint32_t>(off & (n - 1));
   const uint32_t q = tb.q[l];
-  v4u s = ld4(first + b * first_stride + off);
-  for (uint32_t j = 0; j < terms_rest; ++j) {
-    const v4u v = ld4(rest + (b * terms_rest + j) * per + off);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) s[e] = add_mod(s[e], v[e], q);
+  const uint32_t* in_b = inner + b * n2 * ctw;
+  const uint32_t mask = (2u << log_n) - 1;
+  uint32_t g = 1, g4 = 1;
+  for (uint32_t e = 0; e <= w; ++e) g = (g * g1) & mask;   // g1^(1 + w)
+  for (int e = 0; e < 4; ++e) g4 = (g4 * g1) & mask;       // g1^4
+  uint32_t acc = w == 0 ? in_b[off] : 0;
+#pragma unroll 4
+  for (uint32_t j = 1 + w; j < n2; j += 4) {
+    acc = add_mod(acc, tmp[(b * (n2 - 1) + j - 1) * ctw + off], q);
+    if (pl < L) acc = add_mod(acc, in_b[j * ctw + static_cast<size_t>(l) * n + perm_src(c, g, log_n)], q);
+    g = (g * g4) & mask;
   }
-  st4(out + i, s);
+  if (w > 0) part[w - 1][lane] = acc;
+  __syncthreads();
+  if (w == 0) out[i] = add_mod(add_mod(acc, part[0][lane], q), add_mod(part[1][lane], part[2][lane], q), q);
+}
+
+// Batched full-polynomial MAC of the BSGS inner sums, for several inputs that
+// share the plaintexts: inner[b][j] = sum_i pt[j][i] (.) baby[b][i].  A thread
+// (row j, limb l, 4 slots, kBatch inputs) reads each plaintext quad once and
+// applies it to every input of its tile; lazy reduction every 15 products.
+constexpr int kBatch = 4;
+__global__ __launch_bounds__(kThreads) void bsgs_mac_batch_kernel(Tables tb, const uint32_t* __restrict__ pt,
+                                                                  const uint32_t* __restrict__ baby, uint32_t count,
+                                                                  uint32_t n1, uint32_t n2, uint32_t L,
+                                                                  uint32_t* __restrict__ inner) {
+  const uint32_t n = tb.n;
+  const uint32_t per_row = n / (kThreads * 4);
+  const uint32_t tiles = (count + kBatch - 1) / kBatch;
+  // blockIdx.x = ((l * per_row + kb) * n2 + j) * tiles + tile
+  const uint32_t tile = blockIdx.x % tiles;
+  const uint32_t rest = blockIdx.x / tiles;
+  const uint32_t j = rest % n2;
+  const uint32_t lk = rest / n2;
+  const uint32_t l = lk / per_row;
+  const uint32_t k = ((lk % per_row) * kThreads + threadIdx.x) * 4;
+  const uint32_t b0 = tile * kBatch;
+  const uint32_t nb = count - b0 < static_cast<uint32_t>(kBatch) ? count - b0 : kBatch;   // workgroup-uniform
+  const uint32_t q = tb.q[l];
+  const double qr = tb.q_recip[l];
+  const size_t ln = static_cast<size_t>(L) * n, ctw = 2 * ln;
+  const uint32_t* prow = pt + (static_cast<size_t>(j) * n1 * L + l) * n + k;
+  uint64_t a0[kBatch][4], a1[kBatch][4];
+#pragma unroll
+  for (int bb = 0; bb < kBatch; ++bb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) a0[bb][e] = a1[bb][e] = 0;
+  uint32_t i = 0;
+  while (i < n1) {
+    const uint32_t stop = min(n1, i + 15);
+    for (; i < stop; ++i) {
+      const v4u pv = ld4(prow + static_cast<size_t>(i) * ln);
+#pragma unroll
+      for (int bb = 0; bb < kBatch; ++bb) {
+        if (static_cast<uint32_t>(bb) < nb) {
+          const uint32_t* x = baby + (static_cast<size_t>(b0 + bb) * n1 + i) * ctw + static_cast<size_t>(l) * n + k;
+          const v4u x0 = ld4(x), x1 = ld4(x + ln);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            a0[bb][e] += static_cast<uint64_t>(pv[e]) * x0[e];
+            a1[bb][e] += static_cast<uint64_t>(pv[e]) * x1[e];
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int bb = 0; bb < kBatch; ++bb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a0[bb][e] = reduce_u64(a0[bb][e], q, qr);
+        a1[bb][e] = reduce_u64(a1[bb][e], q, qr);
+      }
+  }
+#pragma unroll
+  for (int bb = 0; bb < kBatch; ++bb) {
+    if (static_cast<uint32_t>(bb) < nb) {
+      uint32_t* o = inner + (static_cast<size_t>(b0 + bb) * n2 + j) * ctw + static_cast<size_t>(l) * n + k;
+      st4(o, v4u{static_cast<uint32_t>(a0[bb][0]), static_cast<uint32_t>(a0[bb][1]), static_cast<uint32_t>(a0[bb][2]),
+                 static_cast<uint32_t>(a0[bb][3])});
+      st4(o + ln, v4u{static_cast<uint32_t>(a1[bb][0]), static_cast<uint32_t>(a1[bb][1]),
+                      static_cast<uint32_t>(a1[bb][2]), static_cast<uint32_t>(a1[bb][3])});
+    }
+  }
 }
 
 // Workspace of rotate(): T [inputs][L][N], D [inputs][L][L+1][N],
@@ -318,10 +408,13 @@ hipError_t launch_automorphism(const Tables& t, const uint32_t* in, size_t rows,
 // rotation k acts on input k / plan.per_input with key ksk[k % key_period]
 // ([key_period][L][2][L+1][N]) and is written as element k of out_seq.  Each
 // input is decomposed once (ModUp), however many rotations read it.
+// With out == nullptr the rotations stop after ModDown: u[k] is left in the
+// workspace's tmp region (rot_layout(..).tmp) for a fused consumer.
 hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, uint32_t inputs, uint32_t rotations,
                              RotPlan plan, const uint32_t* ksk, void* workspace, uint32_t* out, Seq out_seq,
                              hipStream_t s) {
   if (rotations == 0) return hipSuccess;
+  if (rotations % plan.key_period != 0) return hipErrorInvalidValue;   // every key serves whole batches
   const uint32_t L = t.L - 1, Lp = L + 1;
   const size_t n = t.n;
   RotWs w = rot_layout(t, inputs, rotations, workspace);
@@ -334,11 +427,11 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
   if ((err = hipGetLastError()) != hipSuccess) return err;
   err = launch_ntt(t, w.D, static_cast<size_t>(inputs) * L * Lp, Lp, false, s);
   if (err != hipSuccess) return err;
-  ks_inner_kernel<<<grid_for(static_cast<size_t>(rotations) * Lp * n / 4), kThreads, 0, s>>>(t, w.D, ksk, L,
-                                                                                            rotations, plan, w.acc);
+  ks_inner_kernel<<<grid_for(static_cast<size_t>(plan.key_period) * Lp * n / 4), kThreads, 0, s>>>(
+      t, w.D, ksk, L, rotations, plan, w.acc);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   err = launch_rescale(t, w.acc, w.tmp, rotations, Lp, w.rs, s);
-  if (err != hipSuccess) return err;
+  if (err != hipSuccess || out == nullptr) return err;
   rot_combine_kernel<<<grid_for(static_cast<size_t>(rotations) * L * n / 4), kThreads, 0, s>>>(
       t, ct, in_seq, w.tmp, L, rotations, plan, out, out_seq);
   return hipGetLastError();
@@ -362,12 +455,12 @@ hipError_t launch_keygen_rotation(const Tables& t, const uint32_t* s_ntt, uint32
 }
 
 // Workspace of the BSGS product for `count` input ciphertexts: baby rotations
-// [count][n1][2][L][N], inner sums [count][n2][2][L][N], giant rotations
-// [count][n2-1][2][L][N], the sum [count][2][L][N], and the largest of the two
-// rotation workspaces and the closing rescale's.
+// [count][n1][2][L][N], inner sums [count][n2][2][L][N], the sum
+// [count][2][L][N], and the largest of the two rotation workspaces and the
+// closing rescale's.
 size_t bsgs_workspace_bytes(const Tables& t, uint32_t count, uint32_t n1, uint32_t n2) {
   const size_t ct = static_cast<size_t>(2) * (t.L - 1) * t.n * 4;
-  const size_t fixed = ct * count * (static_cast<size_t>(n1) + n2 + (n2 - 1) + 1);
+  const size_t fixed = ct * count * (static_cast<size_t>(n1) + n2 + 1);
   size_t scratch = rotate_workspace_bytes(t, count, count * (n1 - 1));
   const size_t rot2 = rotate_workspace_bytes(t, count * (n2 - 1), count * (n2 - 1));
   const size_t rs = rescale_workspace_bytes(t, count, t.L - 1);   // the closing rescale
@@ -395,8 +488,7 @@ hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, 
   const size_t key_words = static_cast<size_t>(L) * 2 * (L + 1) * n;
   uint32_t* baby = static_cast<uint32_t*>(workspace);
   uint32_t* inner = baby + static_cast<size_t>(count) * n1 * ctw;
-  uint32_t* giant = inner + static_cast<size_t>(count) * n2 * ctw;
-  uint32_t* sum = giant + static_cast<size_t>(count) * (n2 - 1) * ctw;
+  uint32_t* sum = inner + static_cast<size_t>(count) * n2 * ctw;
   void* rws = sum + static_cast<size_t>(count) * ctw;
   // baby steps: element 0 of each input's group is the input itself, then its
   // rotations by 1 .. n1-1 (one ModUp per input)
@@ -408,20 +500,28 @@ hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, 
                             Seq{n1 - 1, n1, 1}, s);
     if (err != hipSuccess) return err;
   }
-  // inner sums: one full-polynomial MAC per input
-  for (uint32_t b = 0; b < count; ++b) {
-    err = launch_mac_poly(t, pt, baby + static_cast<size_t>(b) * n1 * ctw, inner + static_cast<size_t>(b) * n2 * ctw,
-                          n2, n1, L, s);
-    if (err != hipSuccess) return err;
+  // inner sums: the full-polynomial MAC (one input), or the batched form that
+  // streams the plaintexts once for every kBatch inputs
+  if (count == 1) {
+    err = launch_mac_poly(t, pt, baby, inner, n2, n1, L, s);
+  } else {
+    const size_t grid = static_cast<size_t>(L) * (n / (kThreads * 4)) * n2 * ((count + kBatch - 1) / kBatch);
+    bsgs_mac_batch_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, s>>>(t, pt, baby, count, n1, n2, L, inner);
+    err = hipGetLastError();
   }
-  // giant steps: inner sum j >= 1 of every input rotated by j n1
+  if (err != hipSuccess) return err;
+  // giant steps: inner sum j >= 1 of every input rotated by j n1 (up to ModDown),
+  // then the fused sum of the rotated terms
+  const uint32_t* u = nullptr;
   if (n2 > 1) {
     RotPlan plan{1, n2 - 1, n1, n1, 0};
     err = launch_rotate_seq(t, inner, Seq{n2 - 1, n2, 1}, count * (n2 - 1), count * (n2 - 1), plan,
-                            ksk + static_cast<size_t>(n1 - 1) * key_words, rws, giant, contiguous(), s);
+                            ksk + static_cast<size_t>(n1 - 1) * key_words, rws, nullptr, contiguous(), s);
     if (err != hipSuccess) return err;
+    u = rot_layout(t, count * (n2 - 1), count * (n2 - 1), rws).tmp;
   }
-  sum_terms_kernel<<<grid_for(count * ctw / 4), kThreads, 0, s>>>(t, inner, n2 * ctw, giant, n2 - 1, L, count, sum);
+  giant_sum_kernel<<<static_cast<uint32_t>(count * ctw / 64), kThreads, 0, s>>>(t, inner, u, L, count, n2,
+                                                                                galois_of(n1, t.log_n), sum);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   return launch_rescale(t, sum, out, count, L, rws, s);
 }

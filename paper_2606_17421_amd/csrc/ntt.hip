@@ -20,11 +20,11 @@ __device__ __forceinline__ size_t phys_row(size_t r, uint32_t limbs, uint32_t gs
   return (r / limbs) * gstride + r % limbs;
 }
 
-template <int LOGN, bool INV>
-__global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSimd) void ntt_whole_kernel(Tables tb, uint32_t* rows,
-                                                                          uint32_t limbs, uint32_t gstride) {
-  using P = typename WholePlan<LOGN>::P;
-  constexpr int LOGE = WholePlan<LOGN>::LOGE;
+template <int LOGN, bool INV, bool LAT>
+__global__ __launch_bounds__((WholePlan<LOGN, LAT>::P::T), (WholePlan<LOGN, LAT>::kWavesPerSimd)) void ntt_whole_kernel(
+    Tables tb, uint32_t* rows, uint32_t limbs, uint32_t gstride) {
+  using P = typename WholePlan<LOGN, LAT>::P;
+  constexpr int LOGE = WholePlan<LOGN, LAT>::LOGE;
   __shared__ uint32_t lds[P::lds_words];
   const size_t r = blockIdx.x;
   const uint32_t l = static_cast<uint32_t>(r % limbs);
@@ -120,15 +120,23 @@ __global__ __launch_bounds__(1 << (kBlkLogB - kBlkLogE)) void ntt16_blocks_kerne
   }
 }
 
+template <int LOGN, bool LAT>
+hipError_t launch_whole_plan(const Tables& t, uint32_t* rows, size_t count, uint32_t limbs, bool inv,
+                             hipStream_t s, uint32_t gs) {
+  using P = typename WholePlan<LOGN, LAT>::P;
+  if (inv)
+    ntt_whole_kernel<LOGN, true, LAT><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs, gs);
+  else
+    ntt_whole_kernel<LOGN, false, LAT><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs, gs);
+  return hipGetLastError();
+}
+
+// Fewer rows than CUs: the latency form (each row has a CU to itself).
 template <int LOGN>
 hipError_t launch_whole(const Tables& t, uint32_t* rows, size_t count, uint32_t limbs, bool inv,
                         hipStream_t s, uint32_t gs) {
-  using P = typename WholePlan<LOGN>::P;
-  if (inv)
-    ntt_whole_kernel<LOGN, true><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs, gs);
-  else
-    ntt_whole_kernel<LOGN, false><<<dim3(static_cast<uint32_t>(count)), P::T, 0, s>>>(t, rows, limbs, gs);
-  return hipGetLastError();
+  if ((LOGN == 13 || LOGN == 14) && count < t.num_cus) return launch_whole_plan<LOGN, true>(t, rows, count, limbs, inv, s, gs);
+  return launch_whole_plan<LOGN, false>(t, rows, count, limbs, inv, s, gs);
 }
 
 hipError_t launch_ntt16(const Tables& t, uint32_t* rows, size_t count, uint32_t limbs, bool inv,

@@ -218,10 +218,13 @@ __device__ __forceinline__ void inv_block(uint32_t (&v)[1 << LOGE], uint32_t t, 
 
 // Per-N choice of residues per thread for whole-polynomial blocks.  Kernels
 // over whole polynomials ask for 4 waves per SIMD (a 128-register budget):
-// two 2^14 workgroups, or one 2^15 workgroup, fill a CU's LDS.
-template <int LOGN>
+// two 2^14 workgroups, or one 2^15 workgroup, fill a CU's LDS.  The latency
+// form (LAT) is for launches with fewer workgroups than CUs, where each
+// transform has a CU to itself: 16 residues per thread at 2^13 and 2^14, so
+// twice the lanes share each transform's chain.
+template <int LOGN, bool LAT = false>
 struct WholePlan {
-  static constexpr int LOGE = LOGN <= 12 ? 4 : 5;
+  static constexpr int LOGE = (LOGN <= 12 || (LAT && LOGN <= 14)) ? 4 : 5;
   using P = Plan<LOGN, LOGE>;
   static constexpr int kWavesPerSimd = 4;
 };

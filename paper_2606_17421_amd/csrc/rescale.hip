@@ -13,7 +13,7 @@
 // decode-size layer), each workgroup instead takes one output limb of one
 // polynomial (kSplit): the inverse transform is repeated per limb, but the
 // chain per workgroup is two transforms instead of limbs, on limbs - 1 times
-// the workgroups.
+// the workgroups, and with the latency plan (more lanes per transform).
 // N = 2^16: three passes through a workspace (see below).
 #include "ntt_core.hpp"
 
@@ -21,10 +21,10 @@ namespace ckks {
 namespace {
 
 template <int LOGN, bool kSplit>
-__global__ __launch_bounds__(WholePlan<LOGN>::P::T, WholePlan<LOGN>::kWavesPerSimd) void rescale_kernel(
+__global__ __launch_bounds__((WholePlan<LOGN, kSplit>::P::T), (WholePlan<LOGN, kSplit>::kWavesPerSimd)) void rescale_kernel(
     Tables tb, const uint32_t* __restrict__ in, uint32_t* __restrict__ out, uint32_t limbs) {
-  using P = typename WholePlan<LOGN>::P;
-  constexpr int LOGE = WholePlan<LOGN>::LOGE;
+  using P = typename WholePlan<LOGN, kSplit>::P;
+  constexpr int LOGE = WholePlan<LOGN, kSplit>::LOGE;
   constexpr int N = P::B;
   __shared__ uint32_t lds[P::lds_words];
   const size_t poly = blockIdx.x;  // ciphertext * 2 + component
@@ -215,7 +215,7 @@ template <int LOGN>
 hipError_t launch_rescale_whole(const Tables& t, const uint32_t* in, uint32_t* out, uint32_t count,
                                 uint32_t limbs, hipStream_t s) {
   if (4 * static_cast<size_t>(count) <= t.num_cus && limbs > 2)
-    rescale_kernel<LOGN, true><<<dim3(2 * count, limbs - 1), WholePlan<LOGN>::P::T, 0, s>>>(t, in, out, limbs);
+    rescale_kernel<LOGN, true><<<dim3(2 * count, limbs - 1), WholePlan<LOGN, true>::P::T, 0, s>>>(t, in, out, limbs);
   else
     rescale_kernel<LOGN, false><<<dim3(2 * count), WholePlan<LOGN>::P::T, 0, s>>>(t, in, out, limbs);
   return hipGetLastError();

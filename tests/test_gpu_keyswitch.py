@@ -97,7 +97,7 @@ def test_rotate_bit_exact(gpu_lib, log_n, L, hoisted, steps):
 
 
 @pytest.mark.parametrize("log_n,L,n1,n2,count", [(10, 2, 4, 4, 2), (11, 3, 3, 5, 1), (10, 3, 1, 4, 1),
-                                                 (10, 2, 4, 1, 1)])
+                                                 (10, 2, 4, 1, 1), (10, 2, 2, 3, 6)])
 def test_bsgs_bit_exact(gpu_lib, log_n, L, n1, n2, count):
     """Any residues: the product is exact modular arithmetic, so uniform plaintexts and
     ciphertexts are compared with the oracle bit for bit."""
