@@ -19,9 +19,15 @@ giant-step split:
   objects; one call takes n1 - 1 baby-step rotations of the input, n2 ct x pt inner
   sums (the full-polynomial MAC), n2 - 1 giant-step rotations, a sum, and one rescale.
 
+Tiling (section 3.3's small-ring tiles, section 6's GEMM tiling experiment): a
+D x K weight matrix cut into a t_o x t_i grid of d x d tiles (d = D / t_o = K / t_i)
+acts on the input cut into t_i sub-vectors, each encrypted on its own; output block i
+is the homomorphic sum over j of the tile products W_ij x_j (ciphertext additions, mod
+q_l per limb), each tile product a BSGS product as above.
+
 Parity: pinned (tests/test_oracle_keyswitch.py) by decrypting and decoding the result
-against numpy's W @ x, and by the plaintext identity of the diagonal split on random
-matrices.
+against numpy's W @ x, by the plaintext identity of the diagonal split on random
+matrices, and (tiles) by decoding the aggregated blocks against W @ x.
 """
 from __future__ import annotations
 
@@ -74,3 +80,30 @@ def matvec(pt, ct, n1: int, keys, qs_p, psis_p, log_n: int) -> np.ndarray:
     for j in range(1, n2):
         acc = (acc + rotate(inner[j], j * n1, keys[j * n1], qs_p, psis_p, log_n)) % q
     return rescale(acc[None], qs, psis_p[:L], log_n)[0]
+
+
+def tile_slots(W, t_o: int, t_i: int, n1: int, slots: int) -> np.ndarray:
+    """Diagonal slot vectors (t_o, t_i, n2, n1, slots) of the d x d tiles of W (D x K)."""
+    W = np.asarray(W, dtype=np.float64)
+    d = W.shape[0] // t_o
+    if W.shape != (t_o * d, t_i * d):
+        raise ValueError("W must be a t_o x t_i grid of square tiles")
+    return np.stack([np.stack([diagonal_slots(W[i * d:(i + 1) * d, j * d:(j + 1) * d], n1, slots)
+                               for j in range(t_i)]) for i in range(t_o)])
+
+
+def tiled_matvec(pt, cts, n1: int, keys, qs_p, psis_p, log_n: int) -> np.ndarray:
+    """Tile products summed per output block: pt (t_o, t_i, n2, n1, L, N), cts (t_i, 2, L, N)
+    (the encrypted input blocks).  Returns (t_o, 2, L-1, N)."""
+    pt = np.asarray(pt)
+    t_o, t_i = pt.shape[:2]
+    L = cts.shape[2]
+    q = np.array(qs_p[:L - 1], dtype=np.uint64)[:, None]
+    out = []
+    for i in range(t_o):
+        acc = None
+        for j in range(t_i):
+            y = matvec(pt[i, j], cts[j], n1, keys, qs_p, psis_p, log_n)
+            acc = y if acc is None else (acc + y) % q
+        out.append(acc)
+    return np.stack(out)

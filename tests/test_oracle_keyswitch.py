@@ -203,3 +203,30 @@ def test_bsgs_matvec_decrypts_to_w_times_x(log_n, L, d, n1):
     dec = np.array(rlwe.decrypt(out, s, qs[:L - 1], psis[:L - 1], log_n), dtype=np.float64)
     y = OE.decode(dec, delta * delta / qs[L - 1], log_n).real
     assert np.max(np.abs(y - bsgs.replicate(W @ x, slots))) < 1e-3
+
+
+def test_tiled_product_decodes_to_w_times_x():
+    """A 2 x 2 grid of 8 x 8 tiles: block i of the output decodes to (W x)[block i]."""
+    log_n, L, n1, t = 6, 3, 4, 2
+    n, qs_p, psis_p, s, st = _chain(log_n, L, 91)
+    qs, psis = qs_p[:L], psis_p[:L]
+    slots, d = n // 2, 8
+    W = st["weights"].normal(0, 0.5, (t * d, t * d))
+    x = st["activations"].normal(0, 1, t * d)
+    delta = 2.0 ** 25
+    tiles = bsgs.tile_slots(W, t, t, n1, slots)                     # (t, t, n2, n1, slots)
+    pt = OE.encode_poly(tiles, delta, qs, psis, log_n)
+    cts = []
+    for j in range(t):
+        m = OE.round_coeffs(OE.encode_coeffs(bsgs.replicate(x[j * d:(j + 1) * d], slots), log_n), delta)
+        cts.append(rlwe.encrypt(m, s, gen.uniform_residues(st["residues"], (), qs, n),
+                                gen.gaussian_error(st["error"], n), qs, psis, log_n))
+    keys = {r: KS.rotation_key(s, r, gen.uniform_residues(st["residues"], (L,), qs_p, n),
+                               gen.gaussian_error(st["error"], (L, n)), qs_p, psis_p, log_n) for r in (1, 2, 3, 4)}
+    out = bsgs.tiled_matvec(pt, np.stack(cts), n1, keys, qs_p, psis_p, log_n)
+    assert out.shape == (t, 2, L - 1, n)
+    y = W @ x
+    for i in range(t):
+        dec = np.array(rlwe.decrypt(out[i], s, qs[:L - 1], psis[:L - 1], log_n), dtype=np.float64)
+        got = OE.decode(dec, delta * delta / qs[L - 1], log_n).real
+        assert np.max(np.abs(got - bsgs.replicate(y[i * d:(i + 1) * d], slots))) < 1e-3
