@@ -262,6 +262,14 @@ int ckks_linear_bsgs(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* ct
 /* Workspace of ckks_linear_bsgs in bytes ((size_t)-1 for an invalid request). */
 size_t ckks_bsgs_workspace_bytes(const ckks_ctx* ctx, uint32_t count, uint32_t n1, uint32_t n2);
 
+/* Homomorphic addition ct_out = ct_a + ct_b of `count` ciphertexts
+ * [count][2][limbs][N] (NTT form, same scale): the aggregation of tile outputs
+ * when a large product is cut into tiles (section 3.3, tiling of large
+ * homomorphic GEMMs).  ct_out may alias ct_a or ct_b exactly (in place), but
+ * must not partially overlap either. */
+int ckks_add(const ckks_ctx* ctx, const uint32_t* ct_a, const uint32_t* ct_b, uint32_t count, uint32_t limbs,
+             uint32_t* ct_out, void* stream);
+
 /* Workspace size in bytes for `op` (ckks_op) with the given sizes; 0 when
  * none is needed; (size_t)-1 for an invalid request. */
 size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b,

@@ -67,6 +67,7 @@ _SIGS = {
     "ckks_rotate": (_i32, [_vp, _vp, _u32, _u32, _u32, _i32, _vp, _vp, _sz, _vp, _vp]),
     "ckks_linear_bsgs": (_i32, [_vp, _vp, _vp, _u32, _u32, _u32, _vp, _vp, _sz, _vp, _vp]),
     "ckks_bsgs_workspace_bytes": (_sz, [_vp, _u32, _u32, _u32]),
+    "ckks_add": (_i32, [_vp, _vp, _vp, _u32, _u32, _vp, _vp]),
     "ckks_workspace_bytes": (_sz, [_vp, _i32, _u32, _u32, _u32]),
     "ckks_rescaled_scale": (_dbl, [_vp, _dbl, _u32]),
     "ckks_last_error": (ctypes.c_char_p, []),
@@ -299,6 +300,12 @@ def ckks_linear_bsgs(ctx: Context, pt, ct_in, count: int, n1: int, n2: int, ksk,
         _ptr(ksk, "ksk", keys * lk * 2 * L * n4, 4, allow_none=keys == 0),
         _ptr(workspace, "workspace", 0, workspace.element_size() if workspace is not None else 1, allow_none=True),
         wb, _ptr(ct_out, "ct_out", count * 2 * (lk - 1) * n4, 4), _stream(stream)), "ckks_linear_bsgs")
+
+
+def ckks_add(ctx: Context, ct_a, ct_b, count: int, limbs: int, ct_out, stream=None) -> None:
+    nb = count * 2 * limbs * ctx.n * 4
+    _check(_lib.ckks_add(ctx.handle, _ptr(ct_a, "ct_a", nb, 4), _ptr(ct_b, "ct_b", nb, 4), count, limbs,
+                         _ptr(ct_out, "ct_out", nb, 4), _stream(stream)), "ckks_add")
 
 
 def empty_workspace(nbytes: int, device: int = 0):

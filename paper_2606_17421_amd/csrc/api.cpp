@@ -719,6 +719,23 @@ int ckks_linear_bsgs(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* ct
   return he == hipSuccess ? ok() : hip_fail(he, "bsgs launch");
 }
 
+int ckks_add(const ckks_ctx* ctx, const uint32_t* ct_a, const uint32_t* ct_b, uint32_t count, uint32_t limbs,
+             uint32_t* ct_out, void* stream) {
+  if (int rc = check_ctx(ctx)) return rc;
+  if (int rc = check_limbs(ctx, limbs, 1)) return rc;
+  if (count == 0) return ok();
+  if (int rc = check_rows(ctx, count, 2 * limbs)) return rc;
+  if (int rc = check_ptr(ct_a, "ct_a")) return rc;
+  if (int rc = check_ptr(ct_b, "ct_b")) return rc;
+  if (int rc = check_ptr(ct_out, "ct_out")) return rc;
+  const size_t bytes = size_t(count) * 2 * limbs * ctx->n * 4;
+  if ((ct_out != ct_a && overlaps(ct_out, bytes, ct_a, bytes)) || (ct_out != ct_b && overlaps(ct_out, bytes, ct_b, bytes)))
+    return fail(CKKS_E_INVALID_ARG, "ct_out partially overlaps an input");
+  DeviceGuard guard(ctx->device);
+  hipError_t he = ckks::launch_ct_add(ctx->t, ct_a, ct_b, count, limbs, ct_out, static_cast<hipStream_t>(stream));
+  return he == hipSuccess ? ok() : hip_fail(he, "add launch");
+}
+
 size_t ckks_workspace_bytes(const ckks_ctx* ctx, int op, uint32_t a, uint32_t b, uint32_t limbs) {
   if (!ctx || limbs < 1 || limbs > ctx->L) return static_cast<size_t>(-1);
   switch (op) {

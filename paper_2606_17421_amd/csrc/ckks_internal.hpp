@@ -163,6 +163,8 @@ hipError_t launch_keygen_rotation(const Tables& t, const uint32_t* s_ntt, uint32
                                   uint32_t keys, const uint32_t* a, const int32_t* e, uint32_t* ksk,
                                   hipStream_t s);
 size_t bsgs_workspace_bytes(const Tables& t, uint32_t count, uint32_t n1, uint32_t n2);
+hipError_t launch_ct_add(const Tables& t, const uint32_t* a, const uint32_t* b, uint32_t count, uint32_t limbs,
+                         uint32_t* out, hipStream_t s);
 hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, uint32_t count, uint32_t n1,
                        uint32_t n2, const uint32_t* ksk, void* workspace, uint32_t* out, hipStream_t s);
 

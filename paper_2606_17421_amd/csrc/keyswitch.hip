@@ -391,7 +391,31 @@ RotWs rot_layout(const Tables& t, uint32_t inputs, uint32_t rotations, void* bas
   return w;
 }
 
+// out = a + b, elementwise mod q_l over ciphertexts [count][2][limbs][N].
+__global__ __launch_bounds__(kThreads) void ct_add_kernel(Tables tb, const uint32_t* __restrict__ a,
+                                                          const uint32_t* __restrict__ b, uint32_t count,
+                                                          uint32_t limbs, uint32_t* __restrict__ out) {
+  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const size_t total = static_cast<size_t>(count) * 2 * limbs << tb.log_n;
+  if (i >= total) return;
+  const uint32_t l = static_cast<uint32_t>((i >> tb.log_n) % limbs);
+  const uint32_t q = tb.q[l];
+  const v4u x = ld4(a + i), y = ld4(b + i);
+  v4u o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = add_mod(x[e], y[e], q);
+  st4(out + i, o);
+}
+
 }  // namespace
+
+hipError_t launch_ct_add(const Tables& t, const uint32_t* a, const uint32_t* b, uint32_t count, uint32_t limbs,
+                         uint32_t* out, hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  ct_add_kernel<<<grid_for((static_cast<size_t>(count) * 2 * limbs << t.log_n) / 4), kThreads, 0, s>>>(t, a, b, count,
+                                                                                                     limbs, out);
+  return hipGetLastError();
+}
 
 size_t rotate_workspace_bytes(const Tables& t, uint32_t inputs, uint32_t rotations) {
   return rot_layout(t, inputs, rotations, nullptr).bytes;

@@ -48,6 +48,7 @@ def test_null_context_is_rejected_without_a_gpu():
     assert lib.ckks_rotate(None, None, 1, 1, 1, 1, None, None, 0, None, None) == ck.CKKS_E_INVALID_ARG
     assert lib.ckks_linear_bsgs(None, None, None, 1, 2, 2, None, None, 0, None, None) == ck.CKKS_E_INVALID_ARG
     assert lib.ckks_bsgs_workspace_bytes(None, 1, 2, 2) == ctypes.c_size_t(-1).value
+    assert lib.ckks_add(None, None, None, 1, 1, None, None) == ck.CKKS_E_INVALID_ARG
     assert lib.ckks_workspace_bytes(None, ck.CKKS_OP_ROTATE, 1, 1, 2) == ctypes.c_size_t(-1).value
     h = ctypes.c_void_p()
     assert lib.ckks_ctx_create(ctypes.byref(h), 9, 2, None, 0) == ck.CKKS_E_INVALID_ARG      # log_n < 10

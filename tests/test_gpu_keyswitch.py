@@ -177,3 +177,41 @@ def test_rotation_argument_errors(gpu_lib):
         ck.ckks_rotate(two, ck.empty_u32((1, 2, 1, n)), 1, 1, 1, True, ck.empty_u32((1, 1, 2, 2, n)), small,
                        ck.empty_u32((1, 2, 1, n)))
     assert ex.value.code == ck.CKKS_E_INVALID_ARG
+
+
+def test_add_bit_exact(gpu_lib):
+    ck = gpu_lib
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, 11, 3, 795)
+    a = gen.uniform_residues(st["residues"], (5, 2), qs_p[:3], n)
+    b = gen.uniform_residues(st["residues"], (5, 2), qs_p[:3], n)
+    q = np.array(qs_p[:3], dtype=np.uint64)[:, None]
+    want = ((a.astype(np.uint64) + b) % q).astype(np.uint32)
+    da, db = ck.to_device(a), ck.to_device(b)
+    out = ck.empty_u32(a.shape)
+    ck.ckks_add(ctx, da, db, 5, 3, out)
+    assert np.array_equal(ck.to_host_u32(out), want)
+    ck.ckks_add(ctx, da, db, 5, 3, da)                                   # in place
+    assert np.array_equal(ck.to_host_u32(da), want)
+
+
+def test_tiled_product_bit_exact(gpu_lib):
+    """A 2 x 3 grid of tiles: per-tile BSGS calls and ciphertext additions on the GPU
+    equal the oracle's tiled product bit for bit (uniform residues)."""
+    ck = gpu_lib
+    log_n, L, n1, n2, t_o, t_i, count = 10, 2, 2, 2, 2, 3, 1
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 797)
+    pt = gen.uniform_residues(st["residues"], (t_o, t_i, n2, n1), qs_p[:L], n)
+    cts = gen.uniform_residues(st["residues"], (t_i, 2), qs_p[:L], n)
+    steps = [1, 2]
+    keys = oracle_keys(st, s, steps, qs_p, psis_p, log_n)
+    d_keys, d_pt, d_ct = ck.to_device(keys), ck.to_device(pt), ck.to_device(cts)
+    ws = ck.empty_workspace(ck.bsgs_workspace_bytes(ctx, count, n1, n2))
+    out = ck.empty_u32((t_o, 2, L - 1, n))
+    part = ck.empty_u32((2, L - 1, n))
+    for i in range(t_o):
+        ck.ckks_linear_bsgs(ctx, d_pt[i, 0], d_ct[0:1], 1, n1, n2, d_keys, ws, out[i])
+        for j in range(1, t_i):
+            ck.ckks_linear_bsgs(ctx, d_pt[i, j], d_ct[j:j + 1], 1, n1, n2, d_keys, ws, part)
+            ck.ckks_add(ctx, out[i], part, 1, L - 1, out[i])
+    want = OB.tiled_matvec(pt, cts.astype(np.uint64), n1, {1: keys[0], 2: keys[1]}, qs_p, psis_p, log_n)
+    assert np.array_equal(ck.to_host_u32(out), want.astype(np.uint32))
