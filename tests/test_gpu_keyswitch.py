@@ -215,3 +215,21 @@ def test_tiled_product_bit_exact(gpu_lib):
             ck.ckks_add(ctx, out[i], part, 1, L - 1, out[i])
     want = OB.tiled_matvec(pt, cts.astype(np.uint64), n1, {1: keys[0], 2: keys[1]}, qs_p, psis_p, log_n)
     assert np.array_equal(ck.to_host_u32(out), want.astype(np.uint32))
+
+
+def test_bsgs_full_size_bit_exact(gpu_lib):
+    """The benchmarked call's shape: d = 1024 (n1 = n2 = 32) at N = 2^13 with 4 ciphertext
+    primes and the special prime, one input; uniform residues, oracle keys, compared with
+    the oracle's product bit for bit."""
+    ck = gpu_lib
+    log_n, L, n1, n2 = 13, 4, 32, 32
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 799)
+    pt = gen.uniform_residues(st["residues"], (n2, n1), qs_p[:L], n)
+    ct = gen.uniform_residues(st["residues"], (1, 2), qs_p[:L], n)
+    steps = list(range(1, n1)) + [j * n1 for j in range(1, n2)]
+    keys = oracle_keys(st, s, steps, qs_p, psis_p, log_n)
+    ws = ck.empty_workspace(ck.bsgs_workspace_bytes(ctx, 1, n1, n2))
+    out = ck.empty_u32((1, 2, L - 1, n))
+    ck.ckks_linear_bsgs(ctx, ck.to_device(pt), ck.to_device(ct), 1, n1, n2, ck.to_device(keys), ws, out)
+    want = OB.matvec(pt, ct[0].astype(np.uint64), n1, {r: keys[i] for i, r in enumerate(steps)}, qs_p, psis_p, log_n)
+    assert np.array_equal(ck.to_host_u32(out)[0], want.astype(np.uint32))
