@@ -234,3 +234,27 @@ def test_bsgs_full_size_bit_exact(gpu_lib):
     ck.ckks_linear_bsgs(ctx, ck.to_device(pt), ck.to_device(ct), 1, n1, n2, ck.to_device(keys), ws, out)
     want = OB.matvec(pt, ct[0].astype(np.uint64), n1, {r: keys[i] for i, r in enumerate(steps)}, qs_p, psis_p, log_n)
     assert np.array_equal(ck.to_host_u32(out)[0], want.astype(np.uint32))
+
+
+def test_add_rejects_partial_overlap(gpu_lib):
+    ck = gpu_lib
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, 10, 2, 801)
+    buf = ck.empty_u32((3, 2, 2, n))
+    with pytest.raises(ck.CkksError) as ex:
+        ck.ckks_add(ctx, buf[0:2], buf[1:3], 2, 2, buf[1:3])   # out aliases b exactly, overlaps a partly
+    assert ex.value.code == ck.CKKS_E_INVALID_ARG
+
+
+def test_bsgs_one_by_one(gpu_lib):
+    """d = 1 (n1 = n2 = 1): no rotations, no keys; the product is pt (.) x, rescaled."""
+    ck = gpu_lib
+    log_n, L = 10, 3
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 803)
+    pt = gen.uniform_residues(st["residues"], (1, 1), qs_p[:L], n)
+    ct = gen.uniform_residues(st["residues"], (2, 2), qs_p[:L], n)
+    ws = ck.empty_workspace(ck.bsgs_workspace_bytes(ctx, 2, 1, 1))
+    out = ck.empty_u32((2, 2, L - 1, n))
+    ck.ckks_linear_bsgs(ctx, ck.to_device(pt), ck.to_device(ct), 2, 1, 1, None, ws, out)
+    for b in range(2):
+        want = OB.matvec(pt, ct[b].astype(np.uint64), 1, {}, qs_p, psis_p, log_n)
+        assert np.array_equal(ck.to_host_u32(out)[b], want.astype(np.uint32))

@@ -193,7 +193,7 @@ def _decode_rows(pt_ntt, qs, psis, log_n, delta):
     return np.array(out)
 
 
-@pytest.mark.parametrize("log_n,limbs,count", [(10, 3, 6), (12, 2, 2), (15, 2, 1)])
+@pytest.mark.parametrize("log_n,limbs,count", [(10, 3, 6), (12, 2, 2), (13, 4, 2), (14, 4, 1), (15, 2, 1)])
 def test_encode_poly_within_tolerance(gpu_lib, log_n, limbs, count):
     ck = gpu_lib
     ctx = ctx_for(ck, log_n, max(limbs, 3))
@@ -220,7 +220,7 @@ def test_encode_poly_within_tolerance(gpu_lib, log_n, limbs, count):
     assert mismatches <= max(2, count * n // 100000)
 
 
-@pytest.mark.parametrize("log_n,limbs", [(10, 3), (15, 2)])
+@pytest.mark.parametrize("log_n,limbs", [(10, 3), (14, 3), (15, 2)])
 def test_encode_poly_large_coefficients(gpu_lib, log_n, limbs):
     """Slots offset by 4.0 at scale 2^30: coefficients beyond 2^31 take the
     encoder's wide path (every limb's coefficient residues written first, then
