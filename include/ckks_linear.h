@@ -50,7 +50,7 @@ typedef struct ckks_ctx ckks_ctx;
 enum ckks_status {
   CKKS_OK = 0,
   CKKS_E_INVALID_ARG = -1, /* bad shape, pointer, alignment or modulus          */
-  CKKS_E_UNSUPPORTED = -2, /* valid request this build does not implement      */
+  CKKS_E_UNSUPPORTED = -2, /* valid request the library does not implement    */
   CKKS_E_HIP = -3,         /* a HIP runtime call or launch failed              */
   CKKS_E_WORKSPACE = -4    /* workspace missing or smaller than required       */
 };
