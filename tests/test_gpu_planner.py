@@ -84,3 +84,43 @@ def test_chain_equals_the_oracle_composition(gpu_lib):
             cur = OR.refresh(cur, s, a, e, qs, psis, LOG_N, L)
     assert got.shape == cur.shape
     assert np.array_equal(got, cur.astype(np.uint32))
+
+
+def test_chain_at_the_benchmarked_width(gpu_lib):
+    """Three groups of the benchmarked stack's width (32 x 32, N = 2^14, 4 limbs, a TEE
+    window after the first), one pinned and two fallback, against the oracle's chain.
+    Constant-slot weights: the NTT form of the constant polynomial round(c scale) is that
+    constant in every slot, so the oracle's plaintexts are its scalar encodings (the
+    equality of the two encodings for constant slots is pinned on the oracle side)."""
+    ck = gpu_lib
+    log_n, L, d = 14, 4, 32
+    ctx = ck.Context(log_n, L)
+    qs, psis, n = ctx.moduli, ctx.roots, ctx.n
+    groups = [LinearGroup(f"g{i}", d, d, tee_after=(i == 0)) for i in range(3)]
+    rng = np.random.default_rng(505)
+    consts = [rng.normal(0, 0.02, (d, d)) for _ in groups]
+    W = [np.repeat(c.reshape(d * d, 1), n // 2, axis=1) for c in consts]
+    st = gen.streams(506, log_n)
+    s = gen.ternary_secret(st["secret"], n)
+    s_res = np.stack([np.mod(s, q) for q in qs]).astype(np.uint32)
+    s_ntt = ck.to_device(s_res)
+    ck.ckks_ntt(ctx, s_ntt, 1, L)
+    a = gen.uniform_residues(st["residues"], (d,), qs, n)
+    e = gen.gaussian_error(st["error"], (d, n)).astype(np.int32)
+    ct = gen.uniform_residues(st["residues"], (d, 2), qs, n)
+    sec = {"s_ntt": s_ntt, "a": ck.to_device(a), "e": ck.to_device(e)}
+    budget = plan(groups, 1 << 40, L, n).steps[0].encoded_bytes           # only the first group fits
+    p = plan(groups, budget, L, n)
+    assert [st_.pinned for st_ in p.steps] == [True, False, False]
+    ex = Executor(ctx, p, [ck.to_device(w) for w in W], SCALE, sec)
+    out, limbs = ex.run(ck.to_device(ct))
+    got = ck.to_host_u32(out[: d * 2 * limbs * n]).reshape(d, 2, limbs, n)
+    cur = ct.astype(np.uint64)
+    for step, c in zip(p.steps, consts):
+        lv = step.level
+        w_enc = OE.encode_scalar(c, SCALE, qs[:lv])                              # (d, d, lv)
+        pt = np.broadcast_to(w_enc[..., None], (d, d, lv, n))
+        cur = OL.rescale(OL.mac_poly(pt, cur, qs[:lv]), qs[:lv], psis[:lv], log_n)
+        if step.refresh_after:
+            cur = OR.refresh(cur, s, a, e, qs, psis, log_n, L)
+    assert np.array_equal(got, cur.astype(np.uint32))
