@@ -258,3 +258,28 @@ def test_bsgs_one_by_one(gpu_lib):
     for b in range(2):
         want = OB.matvec(pt, ct[b].astype(np.uint64), 1, {}, qs_p, psis_p, log_n)
         assert np.array_equal(ck.to_host_u32(out)[b], want.astype(np.uint32))
+
+
+def test_tiled_product_at_the_benchmarked_shape(gpu_lib):
+    """The sweep's 2x2 configuration for one row: 512 x 512 tiles (n1 = 32, n2 = 16) at
+    N = 2^12, four limbs and the special prime; per-tile BSGS calls and ciphertext
+    additions equal the oracle's tiled product bit for bit (uniform residues)."""
+    ck = gpu_lib
+    log_n, L, n1, n2, t = 12, 4, 32, 16, 2
+    ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 807)
+    pt = gen.uniform_residues(st["residues"], (t, t, n2, n1), qs_p[:L], n)
+    cts = gen.uniform_residues(st["residues"], (t, 2), qs_p[:L], n)
+    steps = list(range(1, n1)) + [j * n1 for j in range(1, n2)]
+    keys = oracle_keys(st, s, steps, qs_p, psis_p, log_n)
+    d_keys, d_pt, d_ct = ck.to_device(keys), ck.to_device(pt), ck.to_device(cts)
+    ws = ck.empty_workspace(ck.bsgs_workspace_bytes(ctx, 1, n1, n2))
+    out = ck.empty_u32((t, 2, L - 1, n))
+    part = ck.empty_u32((2, L - 1, n))
+    for i in range(t):
+        ck.ckks_linear_bsgs(ctx, d_pt[i, 0], d_ct[0:1], 1, n1, n2, d_keys, ws, out[i])
+        for j in range(1, t):
+            ck.ckks_linear_bsgs(ctx, d_pt[i, j], d_ct[j:j + 1], 1, n1, n2, d_keys, ws, part)
+            ck.ckks_add(ctx, out[i], part, 1, L - 1, out[i])
+    want = OB.tiled_matvec(pt, cts.astype(np.uint64), n1, {r: keys[k] for k, r in enumerate(steps)}, qs_p, psis_p,
+                           log_n)
+    assert np.array_equal(ck.to_host_u32(out), want.astype(np.uint32))
