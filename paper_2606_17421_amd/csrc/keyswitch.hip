@@ -124,6 +124,51 @@ __global__ __launch_bounds__(kThreads) void modup_lift_kernel(Tables tb, const u
   }
 }
 
+// ModUp in one kernel for small launches (N <= 2^14): a workgroup takes
+// digit i of input m and one target prime p_j.  It reads limb i of c1
+// coalesced, inverse-transforms it, centres it (|d| < q_i / 2) and writes
+// NTT_j(d mod p_j) to D[m][i][j]; for j == i that is limb i itself, copied.
+// The same values as the copy / batched INTT / lift / batched NTT route, with
+// a chain of two transforms per workgroup instead of four launches.
+template <int LOGN>
+__global__ __launch_bounds__((WholePlan<LOGN, true>::P::T), (WholePlan<LOGN, true>::kWavesPerSimd)) void
+modup_fused_kernel(Tables tb, const uint32_t* __restrict__ ct, Seq in_seq, uint32_t L, uint32_t* __restrict__ D) {
+  using P = typename WholePlan<LOGN, true>::P;
+  constexpr int LOGE = WholePlan<LOGN, true>::LOGE;
+  constexpr int N = P::B;
+  __shared__ uint32_t lds[P::lds_words];
+  const uint32_t m = blockIdx.x / L, i = blockIdx.x % L, j = blockIdx.y;
+  const uint32_t t = threadIdx.x;
+  const uint32_t Lp = L + 1;
+  const uint32_t c_base = pos_coalesced<LOGE>(t, 0);
+  const uint32_t* src = ct + (seq_pos(m, in_seq) * 2 + 1) * L * N + static_cast<size_t>(i) * N + c_base;
+  uint32_t* dst = D + ((static_cast<size_t>(m) * L + i) * Lp + j) * N + c_base;
+  uint32_t v[P::E];
+#pragma unroll
+  for (int e = 0; e < P::E; ++e) v[e] = src[e << 6];
+  if (j == i) {                                             // workgroup-uniform
+#pragma unroll
+    for (int e = 0; e < P::E; ++e) dst[e << 6] = v[e];
+    return;
+  }
+  wave_relayout<LOGN, LOGE, true>(v, t, lds);
+  const uint32_t qi = tb.q[i];
+  const size_t ti = static_cast<size_t>(i) << LOGN;
+  inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + ti, tb.inv_shoup + ti, qi, lds);
+  const uint32_t ni = tb.ninv[i], nis = tb.ninv_shoup[i];
+  const uint32_t pj = tb.q[j];
+#pragma unroll
+  for (int e = 0; e < P::E; ++e) {
+    const uint32_t y = mul_shoup(v[e], ni, nis, qi);
+    v[e] = y > (qi >> 1) ? pj - (qi - y) : y;               // centred digit mod p_j
+  }
+  const size_t tj = static_cast<size_t>(j) << LOGN;
+  fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tj, tb.fwd_shoup + tj, pj, lds);
+  wave_relayout<LOGN, LOGE, false>(v, t, lds);
+#pragma unroll
+  for (int e = 0; e < P::E; ++e) dst[e << 6] = v[e];
+}
+
 // Key-switch inner product for rotation k (input m, Galois element g):
 //   acc[k][p][j][n] = sum_i D[m][i][j][perm_g(n)] * K[slot][i][p][j][n]   mod p_j,  p in {0, 1}.
 // Products are below 2^60 and at most 15 are summed, so one reduction of the
@@ -442,15 +487,30 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
   const uint32_t L = t.L - 1, Lp = L + 1;
   const size_t n = t.n;
   RotWs w = rot_layout(t, inputs, rotations, workspace);
-  c1_copy_kernel<<<grid_for(inputs * L * n / 4), kThreads, 0, s>>>(t, ct, in_seq, inputs, L, w.T);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  err = launch_ntt(t, w.T, static_cast<size_t>(inputs) * L, L, true, s);
-  if (err != hipSuccess) return err;
-  modup_lift_kernel<<<grid_for(inputs * L * n / 4), kThreads, 0, s>>>(t, w.T, inputs, L, w.D);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
-  err = launch_ntt(t, w.D, static_cast<size_t>(inputs) * L * Lp, Lp, false, s);
-  if (err != hipSuccess) return err;
+  hipError_t err;
+  // ModUp: one fused launch while its workgroups (one per input, digit and prime)
+  // fit the chip once, else copy / batched INTT / lift / batched NTT
+  const size_t fused_groups = static_cast<size_t>(inputs) * L * Lp;
+  if (t.log_n <= 14 && fused_groups <= t.num_cus) {
+    const dim3 grid(inputs * L, Lp);
+    switch (t.log_n) {
+      case 10: modup_fused_kernel<10><<<grid, WholePlan<10, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
+      case 11: modup_fused_kernel<11><<<grid, WholePlan<11, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
+      case 12: modup_fused_kernel<12><<<grid, WholePlan<12, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
+      case 13: modup_fused_kernel<13><<<grid, WholePlan<13, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
+      default: modup_fused_kernel<14><<<grid, WholePlan<14, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
+    }
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+  } else {
+    c1_copy_kernel<<<grid_for(inputs * L * n / 4), kThreads, 0, s>>>(t, ct, in_seq, inputs, L, w.T);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    err = launch_ntt(t, w.T, static_cast<size_t>(inputs) * L, L, true, s);
+    if (err != hipSuccess) return err;
+    modup_lift_kernel<<<grid_for(inputs * L * n / 4), kThreads, 0, s>>>(t, w.T, inputs, L, w.D);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    err = launch_ntt(t, w.D, static_cast<size_t>(inputs) * L * Lp, Lp, false, s);
+    if (err != hipSuccess) return err;
+  }
   ks_inner_kernel<<<grid_for(static_cast<size_t>(plan.key_period) * Lp * n / 4), kThreads, 0, s>>>(
       t, w.D, ksk, L, rotations, plan, w.acc);
   if ((err = hipGetLastError()) != hipSuccess) return err;
