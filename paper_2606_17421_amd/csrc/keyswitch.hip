@@ -489,9 +489,10 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
   RotWs w = rot_layout(t, inputs, rotations, workspace);
   hipError_t err;
   // ModUp: one fused launch while its workgroups (one per input, digit and prime)
-  // fit the chip once, else copy / batched INTT / lift / batched NTT
+  // number at most four per CU (the baby and giant steps of one vector at d = 1024:
+  // 20 and 620), else copy / batched INTT / lift / batched NTT
   const size_t fused_groups = static_cast<size_t>(inputs) * L * Lp;
-  if (t.log_n <= 14 && fused_groups <= t.num_cus) {
+  if (t.log_n <= 14 && fused_groups <= 4 * static_cast<size_t>(t.num_cus)) {
     const dim3 grid(inputs * L, Lp);
     switch (t.log_n) {
       case 10: modup_fused_kernel<10><<<grid, WholePlan<10, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
