@@ -13,8 +13,10 @@
 //
 // Encryption and decryption run the batched NTT kernels over the c0 rows (or
 // the output rows) through their row-group stride, with pointwise passes
-// around them, 16 bytes per thread and limb.  The refresh is one fused kernel
-// per ciphertext up to N = 2^14 and the same pass structure above.
+// around them, 16 bytes per thread and limb.  The refresh, up to N = 2^14, is
+// one fused kernel split by output limb for decode-size counts and two
+// transform kernels (decrypt + inverse, lift + forward + combine) for larger
+// ones; above 2^14 it is the pass structure of encryption and decryption.
 #include "ntt_core.hpp"
 
 namespace ckks {
@@ -162,21 +164,16 @@ __global__ __launch_bounds__(kThreads) void dte_lift_kernel(Tables tb, const int
   }
 }
 
-// Fused refresh for N <= 2^14: one workgroup per ciphertext.  Limbs 0 and
-// 1 of c0 + c1 (.) s are read coalesced and inverse-transformed in LDS; the
-// CRT value over q0 q1 is kept as its two digits x = x0 + q0 k (k with the
+// Fused refresh for N <= 2^14 and at most half as many ciphertexts as CUs (a
+// decode-size group): one workgroup per ciphertext and output limb.  Limbs 0
+// and 1 of c0 + c1 (.) s are read coalesced and inverse-transformed in LDS;
+// the CRT value over q0 q1 is kept as its two digits x = x0 + q0 k (k with the
 // centring flag in bit 31) in the group-0 layout that the forward transform
-// starts from, and per output limb it is rebuilt mod q_l with 32-bit
-// Barrett products, the fresh error added, transformed, combined with a and
-// s and written coalesced.  Row transfers per ciphertext: 4 + limbs_out (a)
-// + limbs_out (error, L2) in, 2 limbs_out out; the multi-pass route moves
-// 13 + 7 limbs_out.
-// 16 residues per thread up to 2^14 (1024 threads) keeps the live state in
-// registers.  With fewer ciphertexts than half the CUs (a decode-size group)
-// each workgroup takes one output limb of one ciphertext (kSplit): the two
-// inverse transforms are repeated per limb, but the chain per workgroup is
-// three transforms instead of 2 + limbs_out, on limbs_out times the
-// workgroups.
+// starts from, rebuilt mod q_l with 32-bit Barrett products, the fresh error
+// added, transformed, combined with a and s and written coalesced.  The two
+// inverse transforms are repeated per output limb, so the chain per workgroup
+// is three transforms on limbs_out times the workgroups.  16 residues per
+// thread (1024 threads at 2^14) keeps the live state in registers.
 template <int LOGN>
 struct RefreshPlan {
   static_assert(LOGN <= 14, "the fused refresh serves N <= 2^14");
@@ -185,7 +182,7 @@ struct RefreshPlan {
   static constexpr int kWavesPerSimd = 4;
 };
 
-template <int LOGN, bool kSplit>
+template <int LOGN>
 __global__ __launch_bounds__(RefreshPlan<LOGN>::P::T, RefreshPlan<LOGN>::kWavesPerSimd) void refresh_kernel(
     Tables tb, const uint32_t* __restrict__ ct_in, uint32_t limbs_in, const uint32_t* __restrict__ s_ntt,
     const uint32_t* __restrict__ a, const int32_t* __restrict__ e, uint32_t limbs_out,
@@ -238,8 +235,8 @@ __global__ __launch_bounds__(RefreshPlan<LOGN>::P::T, RefreshPlan<LOGN>::kWavesP
   }
   // the error row through a buffer resource: the per-j offsets j T are scalar constants
   const auto er = row_rsrc(e + c * N, N);
-  const uint32_t l_begin = kSplit ? blockIdx.y : 0, l_end = kSplit ? blockIdx.y + 1 : limbs_out;
-  for (uint32_t l = l_begin; l < l_end; ++l) {
+  {
+    const uint32_t l = blockIdx.y;
     const uint32_t q = tb.q[l], mu = tb.barrett[l];
     const uint32_t q0l = q0 >= q ? q0 - q : q0, q1l = q1 >= q ? q1 - q : q1;  // q0, q1 < 2q
     const uint32_t q2l = mul_mod_barrett(q0l, q1l, q, mu);                      // q0 q1 mod q
@@ -269,16 +266,124 @@ __global__ __launch_bounds__(RefreshPlan<LOGN>::P::T, RefreshPlan<LOGN>::kWavesP
   }
 }
 
+// Two-kernel refresh for N <= 2^14: the same arithmetic as the fused kernel,
+// with each transform in a workgroup of its own and the whole-row plan's
+// occupancy (two workgroups per CU).
+// (1) per (ciphertext, limb 0 or 1): c0 + c1 (.) s read coalesced, inverse
+//     transform, the coefficient residues written to c1 row 0 / 1 of ct_out
+//     (scratch);
+// (2) per (ciphertext, output limb): the CRT digits of the two scratch rows,
+//     the value mod q_l plus the fresh error, the forward transform, and
+//     c0 = . - a (.) s written coalesced;
+// c1 = a: rows from 2 on by (2), rows 0 and 1 (the scratch) copied afterwards.
+template <int LOGN>
+__global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPerSimd)) void dte_dec_intt_kernel(
+    Tables tb, const uint32_t* __restrict__ ct_in, uint32_t limbs_in, const uint32_t* __restrict__ s_ntt,
+    uint32_t limbs_out, uint32_t* __restrict__ ct_out) {
+  using P = typename WholePlan<LOGN>::P;
+  constexpr int LOGE = WholePlan<LOGN>::LOGE;
+  constexpr int N = P::B;
+  __shared__ uint32_t lds[P::lds_words];
+  const size_t c = blockIdx.x >> 1;
+  const uint32_t l = blockIdx.x & 1, t = threadIdx.x;
+  const uint32_t q = tb.q[l], mu = tb.barrett[l];
+  const uint32_t cb = pos_coalesced<LOGE>(t, 0);
+  const uint32_t* c0 = ct_in + ((c * 2) * limbs_in + l) * N + cb;
+  const uint32_t* c1 = c0 + static_cast<size_t>(limbs_in) * N;
+  const uint32_t* sv = s_ntt + static_cast<size_t>(l) * N + cb;
+  uint32_t v[P::E];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) v[j] = add_mod(c0[j << 6], mul_mod_barrett(c1[j << 6], sv[j << 6], q, mu), q);
+  wave_relayout<LOGN, LOGE, true>(v, t, lds);
+  const size_t tl = static_cast<size_t>(l) << LOGN;
+  inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + tl, tb.inv_shoup + tl, q, lds);
+  const uint32_t ni = tb.ninv[l], nis = tb.ninv_shoup[l];
+  uint32_t* r = ct_out + ((c * 2 + 1) * limbs_out + l) * N;
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) r[P::template pos<0>(t, j)] = mul_shoup(v[j], ni, nis, q);
+}
+
+template <int LOGN>
+__global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPerSimd)) void dte_lift_ntt_kernel(
+    Tables tb, const int32_t* __restrict__ e, const uint32_t* __restrict__ s_ntt, const uint32_t* __restrict__ a,
+    uint32_t limbs_out, uint32_t* __restrict__ ct_out) {
+  using P = typename WholePlan<LOGN>::P;
+  constexpr int LOGE = WholePlan<LOGN>::LOGE;
+  constexpr int N = P::B;
+  __shared__ uint32_t lds[P::lds_words];
+  // logical id = c * limbs_out + l.  Consecutive workgroup ids alternate XCDs, so
+  // each XCD is given a contiguous range of logical ids: the limbs of one
+  // ciphertext then run together on one XCD and read its two scratch rows and
+  // its error row from HBM once, the other limbs from that XCD's L2.
+  const uint32_t G = gridDim.x;
+  uint32_t lid = blockIdx.x;
+  if ((G & 7u) == 0) lid = (lid & 7u) * (G >> 3) + (lid >> 3);
+  const size_t c = lid / limbs_out;
+  const uint32_t l = lid % limbs_out, t = threadIdx.x;
+  const uint32_t* r0 = ct_out + ((c * 2 + 1) * limbs_out) * N;   // scratch: coefficient residues mod q0, q1
+  const uint32_t* r1 = r0 + N;
+  const int32_t* er = e + c * N;
+  const uint32_t q0 = tb.q[0], q1 = tb.q[1];
+  const uint32_t w = tb.qinv[0 * tb.L + 1], ws = tb.qinv_shoup[0 * tb.L + 1];  // q0^-1 mod q1
+  const uint64_t half = static_cast<uint64_t>(q0) * q1 / 2;
+  const uint32_t q = tb.q[l], mu = tb.barrett[l];
+  const uint32_t q0l = q0 >= q ? q0 - q : q0, q1l = q1 >= q ? q1 - q : q1;  // q0, q1 < 2q
+  const uint32_t q2l = mul_mod_barrett(q0l, q1l, q, mu);                      // q0 q1 mod q
+  uint32_t v[P::E];
+  // keeps the element loads below the per-limb constants: scheduled above them,
+  // the loads' live ranges spill registers
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    const uint32_t idx = P::template pos<0>(t, j);
+    const uint32_t x0 = r0[idx];
+    const uint32_t r0m = x0 >= q1 ? x0 - q1 : x0;                            // x0 < q0 < 2 q1
+    const uint32_t k = mul_shoup(sub_mod(r1[idx], r0m, q1), w, ws, q1);
+    const bool neg = static_cast<uint64_t>(x0) + static_cast<uint64_t>(q0) * k > half;
+    const uint32_t x0l = x0 >= q ? x0 - q : x0;
+    uint32_t y = add_mod(x0l, mul_mod_barrett(k, q0l, q, mu), q);
+    if (neg) y = sub_mod(y, q2l, q);
+    const int32_t ev = er[idx];
+    v[j] = ev < 0 ? sub_mod(y, static_cast<uint32_t>(-ev), q) : add_mod(y, static_cast<uint32_t>(ev), q);
+  }
+  const size_t tl = static_cast<size_t>(l) << LOGN;
+  fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+  wave_relayout<LOGN, LOGE, false>(v, t, lds);
+  const uint32_t cb = pos_coalesced<LOGE>(t, 0);
+  const uint32_t* av = a + (c * limbs_out + l) * N + cb;
+  const uint32_t* sv = s_ntt + static_cast<size_t>(l) * N + cb;
+  uint32_t* o = ct_out + ((c * 2) * limbs_out + l) * N + cb;
+  uint32_t* o1 = o + static_cast<size_t>(limbs_out) * N;       // c1 row l (rows 0, 1 are the scratch)
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    const uint32_t ax = av[j << 6];
+    o[j << 6] = sub_mod(v[j], mul_mod_barrett(ax, sv[j << 6], q, mu), q);
+    if (l >= 2) o1[j << 6] = ax;
+  }
+}
+
+template <int LOGN>
+hipError_t launch_refresh_two(const Tables& t, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
+                              const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
+                              uint32_t* ct_out, hipStream_t s) {
+  constexpr uint32_t T = WholePlan<LOGN>::P::T;
+  dte_dec_intt_kernel<LOGN><<<dim3(2 * count), T, 0, s>>>(t, ct_in, limbs_in, s_ntt, limbs_out, ct_out);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  dte_lift_ntt_kernel<LOGN><<<dim3(count * limbs_out), T, 0, s>>>(t, e, s_ntt, a, limbs_out, ct_out);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  // c1 rows 0 and 1 (the scratch) = a rows 0 and 1; the kernel wrote the others
+  const size_t ct_bytes = static_cast<size_t>(2) * limbs_out * t.n * 4, a_bytes = ct_bytes / 2;
+  return hipMemcpy2DAsync(ct_out + static_cast<size_t>(limbs_out) * t.n, ct_bytes, a, a_bytes, 2 * t.n * 4, count,
+                          hipMemcpyDeviceToDevice, s);
+}
+
 template <int LOGN>
 hipError_t launch_refresh_fused(const Tables& t, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
                                 const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
                                 uint32_t* ct_out, hipStream_t s) {
-  if (2 * static_cast<size_t>(count) <= t.num_cus && limbs_out > 1)
-    refresh_kernel<LOGN, true><<<dim3(count, limbs_out), RefreshPlan<LOGN>::P::T, 0, s>>>(t, ct_in, limbs_in, s_ntt, a,
-                                                                                        e, limbs_out, ct_out);
-  else
-    refresh_kernel<LOGN, false><<<dim3(count), RefreshPlan<LOGN>::P::T, 0, s>>>(t, ct_in, limbs_in, s_ntt, a, e,
-                                                                               limbs_out, ct_out);
+  refresh_kernel<LOGN><<<dim3(count, limbs_out), RefreshPlan<LOGN>::P::T, 0, s>>>(t, ct_in, limbs_in, s_ntt, a, e,
+                                                                                 limbs_out, ct_out);
   return hipGetLastError();
 }
 
@@ -312,7 +417,21 @@ hipError_t launch_decrypt(const Tables& t, const uint32_t* ct, const uint32_t* s
 hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
                           const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
                           uint32_t* ct_out, hipStream_t s) {
-  switch (t.log_n) {  // one fused kernel up to 2^14
+  // Up to 2^14: more ciphertexts than half the CUs take the two-kernel route
+  // (768 ciphertexts at 2^14: 0.46 ms against 0.52 ms fused), fewer the fused
+  // kernel split by output limb (32 ciphertexts: the plan step 13.6 ms against
+  // 13.9 ms).
+  if (2 * static_cast<size_t>(count) > t.num_cus) {
+    switch (t.log_n) {
+      case 10: return launch_refresh_two<10>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+      case 11: return launch_refresh_two<11>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+      case 12: return launch_refresh_two<12>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+      case 13: return launch_refresh_two<13>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+      case 14: return launch_refresh_two<14>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+      default: break;
+    }
+  }
+  switch (t.log_n) {
     case 10: return launch_refresh_fused<10>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
     case 11: return launch_refresh_fused<11>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
     case 12: return launch_refresh_fused<12>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
