@@ -78,7 +78,8 @@ def test_keygen_rotation_bit_exact(gpu_lib, log_n, L, r0, r_step, count):
 
 @pytest.mark.parametrize("log_n,L,hoisted,steps", [(10, 2, True, (1, 2, 3)), (10, 3, False, (5, 9)),
                                                    (12, 3, True, (4, 8)), (13, 2, True, (1, 2, 3)),
-                                                   (14, 3, False, (2, 6)), (16, 2, False, (1,))])
+                                                   (14, 3, False, (2, 6)), (16, 2, False, (1,)),
+                                                   (10, 2, True, (511,))])                 # a left rotation by N/2 - 1 = right by 1
 def test_rotate_bit_exact(gpu_lib, log_n, L, hoisted, steps):
     ck = gpu_lib
     ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 740 + log_n + L)
