@@ -142,3 +142,21 @@ def test_rlwe_argument_errors(gpu_lib):
     P = lambda t: ctypes.c_void_p(t.data_ptr())
     assert ck._lib.ckks_encrypt(ctx.handle, None, P(s_ntt), P(d_a), P(d_e), 2, 4, P(big), None) == ck.CKKS_E_INVALID_ARG
     assert "limbs=4" in ck.ckks_last_error()
+
+
+def test_refresh_at_the_benchmarked_size(gpu_lib):
+    """The refresh workload's shape: 768 ciphertexts at N = 2^14 refreshed from 3 to 4
+    limbs (the two-kernel route); 16 sampled ciphertexts compared with the oracle bit
+    for bit."""
+    ck = gpu_lib
+    log_n, L, count = 14, 4, 768
+    ctx, qs, psis, n, st, s, s_ntt, m, e, a = setup(ck, log_n, L, count, 391)
+    ct = gen.uniform_residues(st["residues"], (count, 2), qs[:3], n)       # any residues: exact arithmetic
+    a2 = gen.uniform_residues(st["residues"], (count,), qs, n)
+    e2 = gen.gaussian_error(st["error"], (count, n)).astype(np.int32)
+    out = ck.empty_u32((count, 2, L, n))
+    ck.ckks_refresh(ctx, ck.to_device(ct), 3, s_ntt, ck.to_device(a2), ck.to_device(e2), count, L, out)
+    got = ck.to_host_u32(out)
+    rows = gen.sample_rows(st["sample"], count, count=16)
+    want = OR.refresh(ct[rows].astype(np.uint64), s, a2[rows], e2[rows], qs, psis, log_n, L).astype(np.uint32)
+    assert np.array_equal(got[rows], want)
