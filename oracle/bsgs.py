@@ -18,6 +18,15 @@ giant-step split:
   The plaintexts pt[j, i] = Encode(rot(diag_{j n1 + i}, -j n1)) are the pre-encoded
   objects; one call takes n1 - 1 baby-step rotations of the input, n2 ct x pt inner
   sums (the full-polynomial MAC), n2 - 1 giant-step rotations, a sum, and one rescale.
+* The giant-step rotations are summed before their division by P (a lazy ModDown, as
+  BSGS implementations commonly do): with y_j the inner sums and (a0_j, a1_j) the
+  key-switching inner product of sigma_j(c1 of y_j) over q_0 .. q_{L-1}, P,
+
+      z = ModDown( P y_0 + sum_{j >= 1} ( (P sigma_j(c0 of y_j), 0) + (a0_j, a1_j) ) ),
+
+  which equals the sum of the n2 rotated inner sums up to the rounding of one
+  division by P instead of n2 - 1 of them (P y is exact in the extended basis:
+  ModDown(P y + a) = y + ModDown(a)).  Then z is rescaled once.
 
 Tiling (section 3.3's small-ring tiles, section 6's GEMM tiling experiment): a
 D x K weight matrix cut into a t_o x t_i grid of d x d tiles (d = D / t_o = K / t_i)
@@ -33,7 +42,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .keyswitch import rotate
+from .keyswitch import automorphism_ct, galois_element, keyswitch_ext, rotate
 from .linear import mac_poly, rescale
 
 
@@ -75,11 +84,23 @@ def matvec(pt, ct, n1: int, keys, qs_p, psis_p, log_n: int) -> np.ndarray:
     for i in range(1, n1):
         baby.append(rotate(baby[0], i, keys[i], qs_p, psis_p, log_n))
     inner = mac_poly(pt, np.stack(baby), qs)              # (n2, 2, L, N)
-    q = np.array(qs, dtype=np.uint64)[:, None]
-    acc = inner[0].copy()
+    P = qs_p[-1]
+    qp = np.array(qs_p, dtype=np.uint64)[:, None]
+    ext = np.zeros((2, L + 1, 1 << log_n), dtype=np.uint64)    # over q_0 .. q_{L-1}, P
+
+    def add_times_p(comp, x):                                  # ext[comp] += P x (x over the q_l)
+        for l in range(L):
+            ql = np.uint64(qs[l])
+            ext[comp, l] = (ext[comp, l] + (np.uint64(P % qs[l]) * (np.asarray(x[l], dtype=np.uint64) % ql)) % ql) % ql
+
+    add_times_p(0, inner[0][0])
+    add_times_p(1, inner[0][1])
     for j in range(1, n2):
-        acc = (acc + rotate(inner[j], j * n1, keys[j * n1], qs_p, psis_p, log_n)) % q
-    return rescale(acc[None], qs, psis_p[:L], log_n)[0]
+        sig = automorphism_ct(inner[j], galois_element(j * n1, log_n), qs_p, psis_p, log_n)
+        add_times_p(0, sig[0])
+        ext = (ext + keyswitch_ext(sig[1], keys[j * n1], qs_p, psis_p, log_n)) % qp
+    z = rescale(ext[None], qs_p, psis_p, log_n)[0]              # one division by P
+    return rescale(z[None], qs, psis_p[:L], log_n)[0]
 
 
 def tile_slots(W, t_o: int, t_i: int, n1: int, slots: int) -> np.ndarray:

@@ -127,10 +127,11 @@ def decompose(c, qs, psis, log_n: int):
     return out
 
 
-def keyswitch(c, ksk, qs_p, psis_p, log_n: int) -> np.ndarray:
-    """Switch the NTT-form polynomial c (L, N) over q_0 .. q_{L-1} with ksk (L, 2, L+1, N).
-
-    Returns (u0, u1) (2, L, N) with u0 + u1 s_to = c s_from + small error.
+def keyswitch_ext(c, ksk, qs_p, psis_p, log_n: int) -> np.ndarray:
+    """The key-switching inner product of the NTT-form polynomial c (L, N) over
+    q_0 .. q_{L-1} with ksk (L, 2, L+1, N), before the division by P: returns
+    (a0, a1) (2, L+1, N) over q_0 .. q_{L-1}, P with a0 + a1 s_to = P c s_from +
+    sum_i d_i e_i (mod Q P).
     """
     L = c.shape[0]
     if L != len(qs_p) - 1:
@@ -144,17 +145,32 @@ def keyswitch(c, ksk, qs_p, psis_p, log_n: int) -> np.ndarray:
             d_hat = ntt(_res(digits[i], p), p, ps, log_n)
             for k in range(2):
                 acc[0, k, j] = (acc[0, k, j] + (d_hat * (np.asarray(ksk[i, k, j], dtype=np.uint64) % pp)) % pp) % pp
-    return rescale(acc, qs_p, psis_p, log_n)[0]           # division by P: drop the last prime
+    return acc[0]
+
+
+def keyswitch(c, ksk, qs_p, psis_p, log_n: int) -> np.ndarray:
+    """Switch the NTT-form polynomial c (L, N) over q_0 .. q_{L-1} with ksk (L, 2, L+1, N).
+
+    Returns (u0, u1) (2, L, N) with u0 + u1 s_to = c s_from + small error.
+    """
+    ext = keyswitch_ext(c, ksk, qs_p, psis_p, log_n)
+    return rescale(ext[None], qs_p, psis_p, log_n)[0]     # division by P: drop the last prime
+
+
+def automorphism_ct(ct, g: int, qs, psis, log_n: int) -> np.ndarray:
+    """sigma_g on both components of an NTT-form ciphertext (2, L, N)."""
+    L = ct.shape[1]
+    sig = np.empty((2, L, 1 << log_n), dtype=np.uint64)
+    for c in range(2):
+        for l in range(L):
+            sig[c, l] = automorphism_ntt(ct[c, l], g, qs[l], psis[l], log_n)
+    return sig
 
 
 def rotate(ct, r: int, ksk, qs_p, psis_p, log_n: int) -> np.ndarray:
     """Rotate the slots of an NTT-form ciphertext (2, L, N) left by r, with ksk = rotation_key(s, r)."""
     L = ct.shape[1]
-    g = galois_element(r, log_n)
-    sig = np.empty((2, L, 1 << log_n), dtype=np.uint64)
-    for c in range(2):
-        for l in range(L):
-            sig[c, l] = automorphism_ntt(ct[c, l], g, qs_p[l], psis_p[l], log_n)
+    sig = automorphism_ct(ct, galois_element(r, log_n), qs_p, psis_p, log_n)
     u = keyswitch(sig[1], ksk, qs_p, psis_p, log_n)
     q = np.array(qs_p[:L], dtype=np.uint64)[:, None]
     return np.stack([(sig[0] + u[0]) % q, u[1]])

@@ -230,3 +230,32 @@ def test_tiled_product_decodes_to_w_times_x():
         dec = np.array(rlwe.decrypt(out[i], s, qs[:L - 1], psis[:L - 1], log_n), dtype=np.float64)
         got = OE.decode(dec, delta * delta / qs[L - 1], log_n).real
         assert np.max(np.abs(got - bsgs.replicate(y[i * d:(i + 1) * d], slots))) < 1e-3
+
+
+def test_lazy_giant_sum_matches_the_sum_of_rotations():
+    """The product's giant steps (summed before one division by P) decrypt to the sum of
+    the individually rotated inner sums within the rounding of the divisions: at most
+    n2 - 1 ModDown roundings before the closing rescale, which divides them away, so the
+    two decryptions differ by the closing rescale's own rounding terms only."""
+    from oracle import linear as OL
+    log_n, L, d, n1 = 6, 3, 16, 4
+    n2 = d // n1
+    n, qs_p, psis_p, s, st = _chain(log_n, L, 95)
+    qs, psis = qs_p[:L], psis_p[:L]
+    pt = gen.uniform_residues(st["residues"], (n2, n1), qs, n)
+    ct = gen.uniform_residues(st["residues"], (2,), qs, n)
+    keys = {r: KS.rotation_key(s, r, gen.uniform_residues(st["residues"], (L,), qs_p, n),
+                               gen.gaussian_error(st["error"], (L, n)), qs_p, psis_p, log_n)
+            for r in list(range(1, n1)) + [j * n1 for j in range(1, n2)]}
+    lazy = bsgs.matvec(pt, ct, n1, keys, qs_p, psis_p, log_n)
+    # eager: every giant-step rotation divided by P on its own, then summed
+    baby = [ct.astype(np.uint64)] + [KS.rotate(ct, i, keys[i], qs_p, psis_p, log_n) for i in range(1, n1)]
+    inner = OL.mac_poly(pt, np.stack(baby), qs)
+    q = np.array(qs, dtype=np.uint64)[:, None]
+    acc = inner[0].copy()
+    for j in range(1, n2):
+        acc = (acc + KS.rotate(inner[j], j * n1, keys[j * n1], qs_p, psis_p, log_n)) % q
+    eager = OL.rescale(acc[None], qs, psis[:L], log_n)[0]
+    diff = (np.array(rlwe.decrypt(lazy, s, qs[:L - 1], psis[:L - 1], log_n), dtype=object)
+            - np.array(rlwe.decrypt(eager, s, qs[:L - 1], psis[:L - 1], log_n), dtype=object))
+    assert max(abs(int(x)) for x in diff) <= n                 # |s| rounding terms, well below any real signal
