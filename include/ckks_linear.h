@@ -248,6 +248,9 @@ int ckks_rotate(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t count, uint
  * d-periodically in the slots of each of `count` input ciphertexts ct_in
  * [count][2][Lk][N] (Halevi-Shoup diagonals with the baby-step / giant-step
  * split):  y = sum_j rot( sum_i pt[j][i] (.) rot(x, i), j n1 ), then one rescale.
+ * The giant-step rotations are summed before their division by P: the sum is
+ * formed over the L primes (P times the unrotated term and the rotated c0
+ * parts, plus the key-switching inner products) and divided by P once.
  * pt [n2][n1][Lk][N]: NTT-form encodings of rot(diag_(j n1 + i), -j n1) (the
  * slot vectors diag_k[t] = W[t mod d][(t + k) mod d]; ckks_linear_encode_poly
  * makes them).  ksk: n1 - 1 rotation keys for steps 1 .. n1-1 followed by

@@ -139,6 +139,8 @@ hipError_t launch_mac_poly(const Tables& t, const uint32_t* pt, const uint32_t* 
 size_t rescale_workspace_bytes(const Tables& t, uint32_t count, uint32_t limbs);
 hipError_t launch_rescale(const Tables& t, const uint32_t* ct_in, uint32_t* ct_out, uint32_t count,
                           uint32_t limbs, void* workspace, hipStream_t s);
+hipError_t launch_rescale2(const Tables& t, const uint32_t* ct_in, uint32_t* mid, uint32_t* ct_out, uint32_t count,
+                           uint32_t limbs, void* workspace, hipStream_t s);
 
 hipError_t launch_zero(uint32_t* p, size_t words, hipStream_t s);
 

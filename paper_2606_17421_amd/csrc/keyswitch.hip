@@ -302,41 +302,55 @@ __global__ __launch_bounds__(kThreads) void keygen_err_kernel(Tables tb, const i
   }
 }
 
-// Giant-step sum fused with the rotations' final step: for input b,
-//   out[b] = inner[b][0] + sum_{j=1}^{n2-1} ( (sigma_gj(c0 of inner[b][j]), 0) + u[b][j] ),
-// u[b][j] = tmp[b (n2-1) + j - 1] (ModDown outputs), g_j = g1^j with g1 = 5^n1.
-// A workgroup takes 64 consecutive coefficients; its 4 waves sum the terms
-// j = 1 + w, 5 + w, .. (independent loads in flight) and combine through LDS.
-__global__ __launch_bounds__(kThreads) void giant_sum_kernel(Tables tb, const uint32_t* __restrict__ inner,
-                                                             const uint32_t* __restrict__ tmp, uint32_t L,
+// Giant-step sum in the extended basis q_0 .. q_{L-1}, P, ahead of its one
+// ModDown: for input b,
+//   ext[b] = P ( inner[b][0] + sum_{j>=1} (sigma_gj(c0 of inner[b][j]), 0) ) + sum_{j>=1} acc[b (n2-1) + j - 1],
+// acc[k] [2][L+1][N] the giant rotations' key-switching inner products (P last),
+// g_j = g1^j with g1 = 5^n1.  P y is exact in the extended basis, so one
+// division by P after the sum stands for the n2 - 1 divisions of the rotations.
+// A workgroup takes 64 consecutive coefficients of one row; its 4 waves sum the
+// terms j = 1 + w, 5 + w, .. (independent loads in flight) and combine through LDS.
+__global__ __launch_bounds__(kThreads) void giant_ext_kernel(Tables tb, const uint32_t* __restrict__ inner,
+                                                             const uint32_t* __restrict__ acc, uint32_t L,
                                                              uint32_t count, uint32_t n2, uint32_t g1,
-                                                             uint32_t* __restrict__ out) {
-  __shared__ uint32_t part[3][64];
+                                                             uint32_t* __restrict__ ext) {
+  __shared__ uint32_t part[2][3][64];
   const uint32_t lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const size_t i = static_cast<size_t>(blockIdx.x) * 64 + lane;
-  const uint32_t log_n = tb.log_n, n = tb.n;
-  const size_t ctw = static_cast<size_t>(2) * L * n;
-  const size_t b = i / ctw;                                 // workgroup-uniform (64 | ctw)
+  const uint32_t log_n = tb.log_n, n = tb.n, Lp = L + 1;
+  const size_t ctw = static_cast<size_t>(2) * L * n, extw = static_cast<size_t>(2) * Lp * n;
+  const size_t b = i / extw;                                // workgroup-uniform (64 | N)
   if (b >= count) return;
-  const size_t off = i % ctw;                               // (p * L + l) * N + c
+  const size_t off = i % extw;                              // (p * (L + 1) + l) * N + c
   const uint32_t pl = static_cast<uint32_t>(off >> log_n);
-  const uint32_t l = pl % L, c = static_cast<uint32_t>(off & (n - 1));
+  const uint32_t p = pl / Lp, l = pl % Lp, c = static_cast<uint32_t>(off & (n - 1));
   const uint32_t q = tb.q[l];
+  const bool carries_sigma = p == 0 && l < L;               // rows with the rotated c0 terms
   const uint32_t* in_b = inner + b * n2 * ctw;
+  const uint32_t* acc_b = acc + b * (n2 - 1) * extw + off;
   const uint32_t mask = (2u << log_n) - 1;
   uint32_t g = 1, g4 = 1;
   for (uint32_t e = 0; e <= w; ++e) g = (g * g1) & mask;   // g1^(1 + w)
   for (int e = 0; e < 4; ++e) g4 = (g4 * g1) & mask;       // g1^4
-  uint32_t acc = w == 0 ? in_b[off] : 0;
+  uint32_t sy = (w == 0 && l < L) ? in_b[(static_cast<size_t>(p) * L + l) * n + c] : 0;
+  uint32_t sa = 0;
 #pragma unroll 4
   for (uint32_t j = 1 + w; j < n2; j += 4) {
-    acc = add_mod(acc, tmp[(b * (n2 - 1) + j - 1) * ctw + off], q);
-    if (pl < L) acc = add_mod(acc, in_b[j * ctw + static_cast<size_t>(l) * n + perm_src(c, g, log_n)], q);
+    sa = add_mod(sa, acc_b[(j - 1) * extw], q);
+    if (carries_sigma) sy = add_mod(sy, in_b[j * ctw + static_cast<size_t>(l) * n + perm_src(c, g, log_n)], q);
     g = (g * g4) & mask;
   }
-  if (w > 0) part[w - 1][lane] = acc;
+  if (w > 0) {
+    part[0][w - 1][lane] = sy;
+    part[1][w - 1][lane] = sa;
+  }
   __syncthreads();
-  if (w == 0) out[i] = add_mod(add_mod(acc, part[0][lane], q), add_mod(part[1][lane], part[2][lane], q), q);
+  if (w == 0) {
+    sy = add_mod(add_mod(sy, part[0][0][lane], q), add_mod(part[0][1][lane], part[0][2][lane], q), q);
+    sa = add_mod(add_mod(sa, part[1][0][lane], q), add_mod(part[1][1][lane], part[1][2][lane], q), q);
+    const uint32_t p_mod = tb.q[L] % q;                     // 0 on the P row, where sy is 0 too
+    ext[i] = add_mod(sa, reduce_u64(static_cast<uint64_t>(sy) * p_mod, q, tb.q_recip[l]), q);
+  }
 }
 
 // Batched full-polynomial MAC of the BSGS inner sums, for several inputs that
@@ -477,8 +491,9 @@ hipError_t launch_automorphism(const Tables& t, const uint32_t* in, size_t rows,
 // rotation k acts on input k / plan.per_input with key ksk[k % key_period]
 // ([key_period][L][2][L+1][N]) and is written as element k of out_seq.  Each
 // input is decomposed once (ModUp), however many rotations read it.
-// With out == nullptr the rotations stop after ModDown: u[k] is left in the
-// workspace's tmp region (rot_layout(..).tmp) for a fused consumer.
+// With out == nullptr the rotations stop before ModDown: the key-switching
+// inner product acc[k] ([2][L+1][N], P last) is left in the workspace's acc
+// region (rot_layout(..).acc) for a consumer that sums before dividing by P.
 hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, uint32_t inputs, uint32_t rotations,
                              RotPlan plan, const uint32_t* ksk, void* workspace, uint32_t* out, Seq out_seq,
                              hipStream_t s) {
@@ -514,9 +529,9 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
   }
   ks_inner_kernel<<<grid_for(static_cast<size_t>(plan.key_period) * Lp * n / 4), kThreads, 0, s>>>(
       t, w.D, ksk, L, rotations, plan, w.acc);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
+  if ((err = hipGetLastError()) != hipSuccess || out == nullptr) return err;
   err = launch_rescale(t, w.acc, w.tmp, rotations, Lp, w.rs, s);
-  if (err != hipSuccess || out == nullptr) return err;
+  if (err != hipSuccess) return err;
   rot_combine_kernel<<<grid_for(static_cast<size_t>(rotations) * L * n / 4), kThreads, 0, s>>>(
       t, ct, in_seq, w.tmp, L, rotations, plan, out, out_seq);
   return hipGetLastError();
@@ -540,15 +555,17 @@ hipError_t launch_keygen_rotation(const Tables& t, const uint32_t* s_ntt, uint32
 }
 
 // Workspace of the BSGS product for `count` input ciphertexts: baby rotations
-// [count][n1][2][L][N], inner sums [count][n2][2][L][N], the sum
-// [count][2][L][N], and the largest of the two rotation workspaces and the
-// closing rescale's.
+// [count][n1][2][L][N], inner sums [count][n2][2][L][N], the giant-step sum in
+// the extended basis [count][2][L+1][N], and the largest of the two rotation
+// workspaces and the two closing rescales'.
 size_t bsgs_workspace_bytes(const Tables& t, uint32_t count, uint32_t n1, uint32_t n2) {
   const size_t ct = static_cast<size_t>(2) * (t.L - 1) * t.n * 4;
-  const size_t fixed = ct * count * (static_cast<size_t>(n1) + n2 + 1);
+  const size_t fixed = ct * count * (static_cast<size_t>(n1) + n2) + static_cast<size_t>(2) * t.L * t.n * 4 * count;
   size_t scratch = rotate_workspace_bytes(t, count, count * (n1 - 1));
   const size_t rot2 = rotate_workspace_bytes(t, count * (n2 - 1), count * (n2 - 1));
-  const size_t rs = rescale_workspace_bytes(t, count, t.L - 1);   // the closing rescale
+  size_t rs = rescale_workspace_bytes(t, count, t.L);             // the ModDown of the sum
+  const size_t rs2 = rescale_workspace_bytes(t, count, t.L - 1);  // the closing rescale
+  rs = rs > rs2 ? rs : rs2;
   scratch = scratch > rot2 ? scratch : rot2;
   return fixed + (scratch > rs ? scratch : rs);
 }
@@ -573,8 +590,8 @@ hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, 
   const size_t key_words = static_cast<size_t>(L) * 2 * (L + 1) * n;
   uint32_t* baby = static_cast<uint32_t*>(workspace);
   uint32_t* inner = baby + static_cast<size_t>(count) * n1 * ctw;
-  uint32_t* sum = inner + static_cast<size_t>(count) * n2 * ctw;
-  void* rws = sum + static_cast<size_t>(count) * ctw;
+  uint32_t* ext = inner + static_cast<size_t>(count) * n2 * ctw;
+  void* rws = ext + static_cast<size_t>(count) * 2 * (L + 1) * n;
   // baby steps: element 0 of each input's group is the input itself, then its
   // rotations by 1 .. n1-1 (one ModUp per input)
   hipError_t err = hipMemcpy2DAsync(baby, n1 * ctw * 4, ct, ctw * 4, ctw * 4, count, hipMemcpyDeviceToDevice, s);
@@ -595,20 +612,20 @@ hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, 
     err = hipGetLastError();
   }
   if (err != hipSuccess) return err;
-  // giant steps: inner sum j >= 1 of every input rotated by j n1 (up to ModDown),
-  // then the fused sum of the rotated terms
-  const uint32_t* u = nullptr;
-  if (n2 > 1) {
-    RotPlan plan{1, n2 - 1, n1, n1, 0};
-    err = launch_rotate_seq(t, inner, Seq{n2 - 1, n2, 1}, count * (n2 - 1), count * (n2 - 1), plan,
-                            ksk + static_cast<size_t>(n1 - 1) * key_words, rws, nullptr, contiguous(), s);
-    if (err != hipSuccess) return err;
-    u = rot_layout(t, count * (n2 - 1), count * (n2 - 1), rws).tmp;
-  }
-  giant_sum_kernel<<<static_cast<uint32_t>(count * ctw / 64), kThreads, 0, s>>>(t, inner, u, L, count, n2,
-                                                                                galois_of(n1, t.log_n), sum);
+  if (n2 == 1) return launch_rescale(t, inner, out, count, L, rws, s);
+  // giant steps: inner sum j >= 1 of every input rotated by j n1, up to the
+  // key-switching inner product; the terms summed in the extended basis; its
+  // ModDown and the product's rescale in one launch (at 2^16 two, through the
+  // baby region, free after the MAC)
+  RotPlan plan{1, n2 - 1, n1, n1, 0};
+  err = launch_rotate_seq(t, inner, Seq{n2 - 1, n2, 1}, count * (n2 - 1), count * (n2 - 1), plan,
+                          ksk + static_cast<size_t>(n1 - 1) * key_words, rws, nullptr, contiguous(), s);
+  if (err != hipSuccess) return err;
+  const uint32_t* acc = rot_layout(t, count * (n2 - 1), count * (n2 - 1), rws).acc;
+  giant_ext_kernel<<<static_cast<uint32_t>(count * 2 * (L + 1) * n / 64), kThreads, 0, s>>>(
+      t, inner, acc, L, count, n2, galois_of(n1, t.log_n), ext);
   if ((err = hipGetLastError()) != hipSuccess) return err;
-  return launch_rescale(t, sum, out, count, L, rws, s);
+  return launch_rescale2(t, ext, baby, out, count, L + 1, rws, s);
 }
 
 }  // namespace ckks

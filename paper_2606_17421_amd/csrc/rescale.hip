@@ -82,6 +82,98 @@ __global__ __launch_bounds__((WholePlan<LOGN, kSplit>::P::T), (WholePlan<LOGN, k
   }
 }
 
+// Two rescales in one launch: divide by the last prime q_t (t = limbs - 1) and
+// then by q_u (u = t - 1), dropping both.  With
+//     r1 = centred INTT_t(c_t),
+//     r2 = centred ((INTT_u(c_u) - r1) q_t^-1 mod q_u)   (the coefficients of
+//          the first rescale's limb u),
+// the second rescale's output limb l < u is
+//     ((c_l - NTT_l(r1)) q_t^-1 - NTT_l(r2)) q_u^-1
+//   = (c_l q_t^-1 - NTT_l(r1 q_t^-1 + r2)) q_u^-1     mod q_l,
+// the same residues as the two rescales in turn.  For launches of few
+// polynomials (the key-switched sum of the BSGS giant steps: its division by
+// the special prime, then the product's own rescale): one workgroup per output
+// limb of one polynomial (blockIdx.y = l), three transforms in its chain
+// instead of four over two launches, no intermediate rows.  (A loop over the
+// limbs would hold r1, r2 and the row in registers at once and spill.)
+template <int LOGN>
+__global__ __launch_bounds__((WholePlan<LOGN, true>::P::T), (WholePlan<LOGN, true>::kWavesPerSimd)) void rescale2_kernel(
+    Tables tb, const uint32_t* __restrict__ in, uint32_t* __restrict__ out, uint32_t limbs) {
+  using P = typename WholePlan<LOGN, true>::P;
+  constexpr int LOGE = WholePlan<LOGN, true>::LOGE;
+  constexpr int N = P::B;
+  constexpr bool kCoalesce = LOGN <= 14;
+  __shared__ uint32_t lds[P::lds_words];
+  const size_t poly = blockIdx.x;  // ciphertext * 2 + component
+  const uint32_t t = threadIdx.x;
+  const uint32_t* src = in + poly * limbs * N;
+  uint32_t* dst = out + poly * (limbs - 2) * N;
+  const uint32_t top = limbs - 1, mid = limbs - 2;
+
+  // coefficients of limb m of this polynomial (times N^-1), group-0 layout
+  auto inverse_row = [&](uint32_t m, uint32_t (&v)[P::E]) {
+    if constexpr (kCoalesce) {
+      const uint32_t* sm = src + static_cast<size_t>(m) * N + pos_coalesced<LOGE>(t, 0);
+#pragma unroll
+      for (int j = 0; j < P::E; ++j) v[j] = sm[j << 6];
+      wave_relayout<LOGN, LOGE, true>(v, t, lds);
+    } else {
+#pragma unroll
+      for (int j = 0; j < P::E; ++j) v[j] = src[static_cast<size_t>(m) * N + P::template pos<P::NG - 1>(t, j)];
+    }
+    const size_t tm = static_cast<size_t>(m) << LOGN;
+    const uint32_t qm = tb.q[m];
+    inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + tm, tb.inv_shoup + tm, qm, lds);
+    const uint32_t ni = tb.ninv[m], nis = tb.ninv_shoup[m];
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = mul_shoup(v[j], ni, nis, qm);
+  };
+  auto centred = [](uint32_t x, uint32_t q) {
+    return x > (q >> 1) ? static_cast<int32_t>(x) - static_cast<int32_t>(q) : static_cast<int32_t>(x);
+  };
+  auto lift = [](int32_t r, uint32_t q) {   // |r| < 2^29 < q
+    return static_cast<uint32_t>(r < 0 ? r + static_cast<int32_t>(q) : r);
+  };
+
+  uint32_t v[P::E];
+  int32_t r1[P::E], r2[P::E];
+  inverse_row(top, v);
+  const uint32_t qt = tb.q[top];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) r1[j] = centred(v[j], qt);
+  __syncthreads();  // every wave's reads of the first transform's last exchange are done
+  inverse_row(mid, v);
+  {
+    const uint32_t qu = tb.q[mid];
+    const uint32_t ti = tb.qinv[top * tb.L + mid], tis = tb.qinv_shoup[top * tb.L + mid];
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) r2[j] = centred(mul_shoup(sub_mod(v[j], lift(r1[j], qu), qu), ti, tis, qu), qu);
+  }
+
+  {
+    const uint32_t l = blockIdx.y, q = tb.q[l];
+    const uint32_t ti = tb.qinv[top * tb.L + l], tis = tb.qinv_shoup[top * tb.L + l];
+    const uint32_t ui = tb.qinv[mid * tb.L + l], uis = tb.qinv_shoup[mid * tb.L + l];
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = add_mod(mul_shoup(lift(r1[j], q), ti, tis, q), lift(r2[j], q), q);
+    const size_t tl = static_cast<size_t>(l) << LOGN;
+    fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+    if constexpr (kCoalesce) {
+      wave_relayout<LOGN, LOGE, false>(v, t, lds);
+      const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
+      uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
+#pragma unroll
+      for (int j = 0; j < P::E; ++j) dl[j << 6] = mul_shoup(sub_mod(mul_shoup(sl[j << 6], ti, tis, q), v[j], q), ui, uis, q);
+    } else {
+#pragma unroll
+      for (int j = 0; j < P::E; ++j) {
+        const size_t x = static_cast<size_t>(l) * N + P::template pos<P::NG - 1>(t, j);
+        dst[x] = mul_shoup(sub_mod(mul_shoup(src[x], ti, tis, q), v[j], q), ui, uis, q);
+      }
+    }
+  }
+}
+
 // ---- N = 2^16: three passes over a chunk of polynomials --------------------
 // A row of 2^16 residues (256 KiB) exceeds the LDS, so each transform splits
 // into a column pass over the top 6 index bits (64 residues per thread,
@@ -242,6 +334,29 @@ hipError_t launch_rescale(const Tables& t, const uint32_t* ct_in, uint32_t* ct_o
     case 16: return rescale16(t, ct_in, ct_out, count, limbs, workspace, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+// Two rescales in turn (limbs -> limbs - 2): one launch of rescale2_kernel for
+// fewer than num_cus / 4 ciphertexts up to 2^15, else the two rescales with
+// the intermediate [count][2][limbs-1][N] in `mid` (caller-provided).
+hipError_t launch_rescale2(const Tables& t, const uint32_t* ct_in, uint32_t* mid, uint32_t* ct_out, uint32_t count,
+                           uint32_t limbs, void* workspace, hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  if (limbs < 3) return hipErrorInvalidValue;
+  if (t.log_n <= 15 && 4 * static_cast<size_t>(count) <= t.num_cus) {
+    const dim3 grid(2 * count, limbs - 2);
+    switch (t.log_n) {
+      case 10: rescale2_kernel<10><<<grid, WholePlan<10, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
+      case 11: rescale2_kernel<11><<<grid, WholePlan<11, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
+      case 12: rescale2_kernel<12><<<grid, WholePlan<12, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
+      case 13: rescale2_kernel<13><<<grid, WholePlan<13, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
+      case 14: rescale2_kernel<14><<<grid, WholePlan<14, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
+      default: rescale2_kernel<15><<<grid, WholePlan<15, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
+    }
+    return hipGetLastError();
+  }
+  const hipError_t err = launch_rescale(t, ct_in, mid, count, limbs, workspace, s);
+  return err != hipSuccess ? err : launch_rescale(t, mid, ct_out, count, limbs - 1, workspace, s);
 }
 
 }  // namespace ckks
