@@ -169,6 +169,74 @@ modup_fused_kernel(Tables tb, const uint32_t* __restrict__ ct, Seq in_seq, uint3
   for (int e = 0; e < P::E; ++e) dst[e << 6] = v[e];
 }
 
+// ModUp in two launches for larger batches (N <= 2^14), without the
+// round trips of the copy / batched INTT / lift / batched NTT route:
+//   modup_intt_kernel, one workgroup per digit (input m, limb i of c1): read
+//     the limb coalesced, inverse-transform it, scale by N^-1 and write the
+//     coefficients to T[m][i] in the plan's group-0 register order (element e
+//     of thread t at e * T + t: coalesced both ways, read back by the same
+//     plan's threads);
+//   modup_ntt_kernel, one workgroup per (digit, prime p_j): centre the digit,
+//     lift it to p_j and forward-transform it into D[m][i][j] (for j == i the
+//     limb itself, copied).
+// One inverse transform per digit instead of one per (digit, prime) as in
+// modup_fused_kernel, whose workgroups then outnumber the CUs.
+template <int LOGN>
+__global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPerSimd)) void modup_intt_kernel(
+    Tables tb, const uint32_t* __restrict__ ct, Seq in_seq, uint32_t L, uint32_t* __restrict__ T) {
+  using P = typename WholePlan<LOGN>::P;
+  constexpr int LOGE = WholePlan<LOGN>::LOGE;
+  constexpr int N = P::B;
+  __shared__ uint32_t lds[P::lds_words];
+  const uint32_t m = blockIdx.x / L, i = blockIdx.x % L;
+  const uint32_t t = threadIdx.x;
+  const uint32_t* src = ct + (seq_pos(m, in_seq) * 2 + 1) * L * N + static_cast<size_t>(i) * N + pos_coalesced<LOGE>(t, 0);
+  uint32_t v[P::E];
+#pragma unroll
+  for (int e = 0; e < P::E; ++e) v[e] = src[e << 6];
+  wave_relayout<LOGN, LOGE, true>(v, t, lds);
+  const uint32_t qi = tb.q[i];
+  const size_t ti = static_cast<size_t>(i) << LOGN;
+  inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + ti, tb.inv_shoup + ti, qi, lds);
+  const uint32_t ni = tb.ninv[i], nis = tb.ninv_shoup[i];
+  uint32_t* dst = T + static_cast<size_t>(blockIdx.x) * N + t;
+#pragma unroll
+  for (int e = 0; e < P::E; ++e) dst[e * P::T] = mul_shoup(v[e], ni, nis, qi);
+}
+
+template <int LOGN>
+__global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPerSimd)) void modup_ntt_kernel(
+    Tables tb, const uint32_t* __restrict__ ct, Seq in_seq, const uint32_t* __restrict__ T, uint32_t L,
+    uint32_t* __restrict__ D) {
+  using P = typename WholePlan<LOGN>::P;
+  constexpr int LOGE = WholePlan<LOGN>::LOGE;
+  constexpr int N = P::B;
+  __shared__ uint32_t lds[P::lds_words];
+  const uint32_t m = blockIdx.x / L, i = blockIdx.x % L, j = blockIdx.y;
+  const uint32_t t = threadIdx.x;
+  const uint32_t c_base = pos_coalesced<LOGE>(t, 0);
+  uint32_t* dst = D + ((static_cast<size_t>(m) * L + i) * (L + 1) + j) * N + c_base;
+  uint32_t v[P::E];
+  if (j == i) {                                             // workgroup-uniform
+    const uint32_t* src = ct + (seq_pos(m, in_seq) * 2 + 1) * L * N + static_cast<size_t>(i) * N + c_base;
+#pragma unroll
+    for (int e = 0; e < P::E; ++e) dst[e << 6] = src[e << 6];
+    return;
+  }
+  const uint32_t* src = T + static_cast<size_t>(blockIdx.x) * N + t;
+  const uint32_t qi = tb.q[i], pj = tb.q[j];
+#pragma unroll
+  for (int e = 0; e < P::E; ++e) {
+    const uint32_t y = src[e * P::T];
+    v[e] = y > (qi >> 1) ? pj - (qi - y) : y;               // centred digit mod p_j
+  }
+  const size_t tj = static_cast<size_t>(j) << LOGN;
+  fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tj, tb.fwd_shoup + tj, pj, lds);
+  wave_relayout<LOGN, LOGE, false>(v, t, lds);
+#pragma unroll
+  for (int e = 0; e < P::E; ++e) dst[e << 6] = v[e];
+}
+
 // Key-switch inner product for rotation k (input m, Galois element g):
 //   acc[k][p][j][n] = sum_i D[m][i][j][perm_g(n)] * K[slot][i][p][j][n]   mod p_j,  p in {0, 1}.
 // Products are below 2^60 and at most 15 are summed, so one reduction of the
@@ -246,6 +314,75 @@ __global__ __launch_bounds__(kThreads) void rot_combine_kernel(Tables tb, const 
   uint32_t* dst = out + seq_pos(k, out_seq) * ctw + static_cast<size_t>(l) * n + c;
   st4(dst, o);
   st4(dst + static_cast<size_t>(L) * n, u1);
+}
+
+// ModDown of the key-switching inner products fused with the rotations' final
+// step (N <= 2^14): for rotation k (input m, Galois element g) and component p,
+//     r   = centred INTT_P(acc[k][p][P row]),
+//     u_l = (acc[k][p][l] - NTT_l(r mod q_l)) P^-1   mod q_l,
+//     out[k] = (sigma_g(c0_m) + u0, u1),
+// the rescale's arithmetic (the P row is the last of the L + 1) with the
+// combine as its store, so u never goes through memory.  For few rotations
+// (the baby steps of one vector): one workgroup per polynomial acc[k][p] and
+// output limb l (blockIdx.y), latency plan, as the split rescale.  (A loop over
+// the limbs would spill with the permuted c0 loads in its store.)
+template <int LOGN>
+__global__ __launch_bounds__((WholePlan<LOGN, true>::P::T), (WholePlan<LOGN, true>::kWavesPerSimd)) void
+moddown_combine_kernel(Tables tb, const uint32_t* __restrict__ acc, const uint32_t* __restrict__ ct, Seq in_seq,
+                       uint32_t L, RotPlan plan, uint32_t* __restrict__ out, Seq out_seq) {
+  using P = typename WholePlan<LOGN, true>::P;
+  constexpr int LOGE = WholePlan<LOGN, true>::LOGE;
+  constexpr int N = P::B;
+  __shared__ uint32_t lds[P::lds_words];
+  const uint32_t poly = blockIdx.x;                         // k * 2 + p
+  const uint32_t k = poly >> 1, p = poly & 1;
+  const uint32_t t = threadIdx.x;
+  const uint32_t top = L;                                   // the special prime's row
+  const uint32_t c_base = pos_coalesced<LOGE>(t, 0);
+  const uint32_t* src = acc + static_cast<size_t>(poly) * (L + 1) * N + c_base;
+  const RotIndex x = rot_index(k, plan, LOGN);
+  const size_t ctw = static_cast<size_t>(2) * L * N;
+  const uint32_t* c0 = ct + seq_pos(x.m, in_seq) * ctw;
+  uint32_t* dst = out + seq_pos(k, out_seq) * ctw + static_cast<size_t>(p) * L * N + c_base;
+
+  uint32_t v[P::E];
+  const uint32_t* stop = src + static_cast<size_t>(top) * N;
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) v[j] = stop[j << 6];
+  wave_relayout<LOGN, LOGE, true>(v, t, lds);
+  const uint32_t qt = tb.q[top];
+  const size_t ttop = static_cast<size_t>(top) << LOGN;
+  inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + ttop, tb.inv_shoup + ttop, qt, lds);
+  const uint32_t ni = tb.ninv[top], nis = tb.ninv_shoup[top];
+  int32_t r[P::E];
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    const uint32_t y = mul_shoup(v[j], ni, nis, qt);
+    r[j] = y > (qt >> 1) ? static_cast<int32_t>(y) - static_cast<int32_t>(qt) : static_cast<int32_t>(y);
+  }
+
+  {
+    const uint32_t l = blockIdx.y, q = tb.q[l];
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = static_cast<uint32_t>(r[j] < 0 ? r[j] + static_cast<int32_t>(q) : r[j]);
+    const size_t tl = static_cast<size_t>(l) << LOGN;
+    fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+    wave_relayout<LOGN, LOGE, false>(v, t, lds);
+    const uint32_t pi = tb.qinv[top * tb.L + l], pis = tb.qinv_shoup[top * tb.L + l];
+    const uint32_t* sl = src + static_cast<size_t>(l) * N;
+    uint32_t* dl = dst + static_cast<size_t>(l) * N;
+    if (p == 0) {                                           // workgroup-uniform
+      const uint32_t* c0l = c0 + static_cast<size_t>(l) * N;
+#pragma unroll
+      for (int j = 0; j < P::E; ++j) {
+        const uint32_t u = mul_shoup(sub_mod(sl[j << 6], v[j], q), pi, pis, q);
+        dl[j << 6] = add_mod(u, c0l[perm_src(c_base + (j << 6), x.g, LOGN)], q);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < P::E; ++j) dl[j << 6] = mul_shoup(sub_mod(sl[j << 6], v[j], q), pi, pis, q);
+    }
+  }
 }
 
 // Rotation keys, after the error rows have been forward-transformed in the
@@ -504,17 +641,34 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
   RotWs w = rot_layout(t, inputs, rotations, workspace);
   hipError_t err;
   // ModUp: one fused launch while its workgroups (one per input, digit and prime)
-  // number at most four per CU (the baby and giant steps of one vector at d = 1024:
-  // 20 and 620), else copy / batched INTT / lift / batched NTT
+  // number at most one per CU (the baby steps of one vector at d = 1024: 20),
+  // else up to 2^14 the two-launch form (the giant steps: 124 inverse and 620
+  // forward workgroups), else copy / batched INTT / lift / batched NTT
   const size_t fused_groups = static_cast<size_t>(inputs) * L * Lp;
-  if (t.log_n <= 14 && fused_groups <= 4 * static_cast<size_t>(t.num_cus)) {
-    const dim3 grid(inputs * L, Lp);
+  const dim3 grid(inputs * L, Lp);
+  if (t.log_n <= 14 && fused_groups <= static_cast<size_t>(t.num_cus)) {
     switch (t.log_n) {
       case 10: modup_fused_kernel<10><<<grid, WholePlan<10, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
       case 11: modup_fused_kernel<11><<<grid, WholePlan<11, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
       case 12: modup_fused_kernel<12><<<grid, WholePlan<12, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
       case 13: modup_fused_kernel<13><<<grid, WholePlan<13, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
       default: modup_fused_kernel<14><<<grid, WholePlan<14, true>::P::T, 0, s>>>(t, ct, in_seq, L, w.D); break;
+    }
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+  } else if (t.log_n <= 14) {
+    switch (t.log_n) {
+#define CKKS_MODUP2(LN)                                                                           \
+  case LN:                                                                                        \
+    modup_intt_kernel<LN><<<inputs * L, WholePlan<LN>::P::T, 0, s>>>(t, ct, in_seq, L, w.T);      \
+    if ((err = hipGetLastError()) != hipSuccess) return err;                                      \
+    modup_ntt_kernel<LN><<<grid, WholePlan<LN>::P::T, 0, s>>>(t, ct, in_seq, w.T, L, w.D);        \
+    break;
+      CKKS_MODUP2(10)
+      CKKS_MODUP2(11)
+      CKKS_MODUP2(12)
+      CKKS_MODUP2(13)
+      default: CKKS_MODUP2(14)
+#undef CKKS_MODUP2
     }
     if ((err = hipGetLastError()) != hipSuccess) return err;
   } else {
@@ -530,6 +684,23 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
   ks_inner_kernel<<<grid_for(static_cast<size_t>(plan.key_period) * Lp * n / 4), kThreads, 0, s>>>(
       t, w.D, ksk, L, rotations, plan, w.acc);
   if ((err = hipGetLastError()) != hipSuccess || out == nullptr) return err;
+  if (t.log_n <= 14 && 4 * static_cast<size_t>(rotations) <= t.num_cus) {
+    const dim3 grid(2 * rotations, L);
+    switch (t.log_n) {
+#define CKKS_MDC(LN)                                                                                       \
+  case LN:                                                                                                 \
+    moddown_combine_kernel<LN><<<grid, WholePlan<LN, true>::P::T, 0, s>>>(t, w.acc, ct, in_seq, L, plan, out, \
+                                                                          out_seq);                        \
+    break;
+      CKKS_MDC(10)
+      CKKS_MDC(11)
+      CKKS_MDC(12)
+      CKKS_MDC(13)
+      default: CKKS_MDC(14)
+#undef CKKS_MDC
+    }
+    return hipGetLastError();
+  }
   err = launch_rescale(t, w.acc, w.tmp, rotations, Lp, w.rs, s);
   if (err != hipSuccess) return err;
   rot_combine_kernel<<<grid_for(static_cast<size_t>(rotations) * L * n / 4), kThreads, 0, s>>>(
