@@ -243,12 +243,16 @@ __global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPe
 // 64-bit sums finishes.  A thread serves one key slot and loops over the
 // rotations that use that key (k = u * key_period + slot, one per input of a
 // batch), so each key is streamed from HBM once per call and re-read from
-// cache by the same thread.
+// cache by the same thread.  When keys x primes x N/4 threads are too few to
+// fill the chip (small rings, large batches), the loop over u is cut into
+// `chunks` ranges on as many workgroups (blockIdx.x / blocks_per_chunk).
 __global__ __launch_bounds__(kThreads) void ks_inner_kernel(Tables tb, const uint32_t* __restrict__ D,
                                                             const uint32_t* __restrict__ ksk, uint32_t L,
                                                             uint32_t rotations, RotPlan plan,
+                                                            uint32_t blocks_per_chunk, uint32_t chunks,
                                                             uint32_t* __restrict__ acc) {
-  const size_t i = (static_cast<size_t>(blockIdx.x) * kThreads + threadIdx.x) * 4;
+  const uint32_t chunk = blockIdx.x / blocks_per_chunk;
+  const size_t i = (static_cast<size_t>(blockIdx.x % blocks_per_chunk) * kThreads + threadIdx.x) * 4;
   const uint32_t log_n = tb.log_n, n = tb.n;
   const size_t row = i >> log_n;                           // slot * (L + 1) + j
   const uint32_t Lp = L + 1;
@@ -263,7 +267,10 @@ __global__ __launch_bounds__(kThreads) void ks_inner_kernel(Tables tb, const uin
   const uint32_t* key = ksk + static_cast<size_t>(slot) * L * key_stride + static_cast<size_t>(j) * n + c;
   const uint32_t pj = tb.q[j];
   const double pr = tb.q_recip[j];
-  for (uint32_t k = slot; k < rotations; k += plan.key_period) {
+  const uint32_t uses = rotations / plan.key_period;        // rotations per key
+  const uint32_t u_begin = static_cast<uint32_t>(static_cast<uint64_t>(uses) * chunk / chunks);
+  const uint32_t u_end = static_cast<uint32_t>(static_cast<uint64_t>(uses) * (chunk + 1) / chunks);
+  for (uint32_t k = slot + u_begin * plan.key_period; k < u_end * plan.key_period; k += plan.key_period) {
     const uint32_t m = k / plan.per_input;
     const uint32_t* dig = D + (static_cast<size_t>(m) * L * Lp + j) * n;
     uint64_t a0[4] = {0, 0, 0, 0}, a1[4] = {0, 0, 0, 0};
@@ -681,8 +688,14 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
     err = launch_ntt(t, w.D, static_cast<size_t>(inputs) * L * Lp, Lp, false, s);
     if (err != hipSuccess) return err;
   }
-  ks_inner_kernel<<<grid_for(static_cast<size_t>(plan.key_period) * Lp * n / 4), kThreads, 0, s>>>(
-      t, w.D, ksk, L, rotations, plan, w.acc);
+  {
+    // every key's uses split over enough workgroups for about 4 per CU
+    const uint32_t blocks = grid_for(static_cast<size_t>(plan.key_period) * Lp * n / 4);
+    const uint32_t uses = rotations / plan.key_period;
+    const uint32_t want = (4 * t.num_cus + blocks - 1) / blocks;
+    const uint32_t chunks = want < 1 ? 1 : (want > uses ? uses : want);
+    ks_inner_kernel<<<blocks * chunks, kThreads, 0, s>>>(t, w.D, ksk, L, rotations, plan, blocks, chunks, w.acc);
+  }
   if ((err = hipGetLastError()) != hipSuccess || out == nullptr) return err;
   if (t.log_n <= 14 && 4 * static_cast<size_t>(rotations) <= t.num_cus) {
     const dim3 grid(2 * rotations, L);
