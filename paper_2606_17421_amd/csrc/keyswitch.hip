@@ -498,69 +498,80 @@ __global__ __launch_bounds__(kThreads) void giant_ext_kernel(Tables tb, const ui
 }
 
 // Batched full-polynomial MAC of the BSGS inner sums, for several inputs that
-// share the plaintexts: inner[b][j] = sum_i pt[j][i] (.) baby[b][i].  A thread
-// (row j, limb l, 4 slots, kBatch inputs) reads each plaintext quad once and
-// applies it to every input of its tile; lazy reduction every 15 products.
-constexpr int kBatch = 4;
-__global__ __launch_bounds__(kThreads) void bsgs_mac_batch_kernel(Tables tb, const uint32_t* __restrict__ pt,
-                                                                  const uint32_t* __restrict__ baby, uint32_t count,
-                                                                  uint32_t n1, uint32_t n2, uint32_t L,
-                                                                  uint32_t* __restrict__ inner) {
+// share the plaintexts: inner[b][j] = sum_i pt[j][i] (.) baby[b][i], per
+// coefficient a (n2 x n1) by (n1 x 2 count) product.  A thread takes one
+// coefficient of one limb and a register tile of kTileJ rows j by kTileB
+// inputs b (both components): per i it loads kTileJ plaintext residues and
+// 2 kTileB input residues for 2 kTileJ kTileB products, so the plaintexts are
+// read count / kTileB times and the inputs n2 / kTileJ times (the previous
+// form, one row by four inputs, re-read every input n2 times and was bound by
+// that L2 traffic).  64-bit sums, reduced every 15 products.  Workgroups that
+// share a plaintext tile (consecutive b tiles) or an input tile are numbered
+// together and placed on one XCD.
+constexpr int kTileJ = 8, kTileB = 2;
+__global__ __launch_bounds__(kThreads) void bsgs_mac_tile_kernel(Tables tb, const uint32_t* __restrict__ pt,
+                                                                 const uint32_t* __restrict__ baby, uint32_t count,
+                                                                 uint32_t n1, uint32_t n2, uint32_t L,
+                                                                 uint32_t* __restrict__ inner) {
   const uint32_t n = tb.n;
-  const uint32_t per_row = n / (kThreads * 4);
-  const uint32_t tiles = (count + kBatch - 1) / kBatch;
-  // blockIdx.x = ((l * per_row + kb) * n2 + j) * tiles + tile
-  const uint32_t tile = blockIdx.x % tiles;
-  const uint32_t rest = blockIdx.x / tiles;
-  const uint32_t j = rest % n2;
-  const uint32_t lk = rest / n2;
-  const uint32_t l = lk / per_row;
-  const uint32_t k = ((lk % per_row) * kThreads + threadIdx.x) * 4;
-  const uint32_t b0 = tile * kBatch;
-  const uint32_t nb = count - b0 < static_cast<uint32_t>(kBatch) ? count - b0 : kBatch;   // workgroup-uniform
+  const uint32_t G = gridDim.x, bid = blockIdx.x;
+  const uint32_t lid = (G & 7) ? bid : (bid & 7) * (G >> 3) + (bid >> 3);   // XCD-contiguous numbering
+  const uint32_t btiles = (count + kTileB - 1) / kTileB, jtiles = (n2 + kTileJ - 1) / kTileJ;
+  const uint32_t cblocks = n / kThreads;
+  // lid = ((l * cblocks + cb) * jtiles + jt) * btiles + bt
+  const uint32_t bt = lid % btiles;
+  uint32_t rest = lid / btiles;
+  const uint32_t jt = rest % jtiles;
+  rest /= jtiles;
+  const uint32_t cb = rest % cblocks, l = rest / cblocks;
+  const uint32_t c = cb * kThreads + threadIdx.x;
+  const uint32_t j0 = jt * kTileJ, b0 = bt * kTileB;
+  const uint32_t jn = n2 - j0 < static_cast<uint32_t>(kTileJ) ? n2 - j0 : kTileJ;   // workgroup-uniform
+  const uint32_t bn = count - b0 < static_cast<uint32_t>(kTileB) ? count - b0 : kTileB;
   const uint32_t q = tb.q[l];
   const double qr = tb.q_recip[l];
   const size_t ln = static_cast<size_t>(L) * n, ctw = 2 * ln;
-  const uint32_t* prow = pt + (static_cast<size_t>(j) * n1 * L + l) * n + k;
-  uint64_t a0[kBatch][4], a1[kBatch][4];
+  const uint32_t* prow = pt + (static_cast<size_t>(j0) * n1 * L + l) * n + c;       // + (jj n1 + i) L N
+  const uint32_t* xrow = baby + static_cast<size_t>(b0) * n1 * ctw + static_cast<size_t>(l) * n + c;   // + (bb n1 + i) ctw
+  const size_t pj_stride = static_cast<size_t>(n1) * ln, xb_stride = static_cast<size_t>(n1) * ctw;
+  uint64_t a[kTileJ][2 * kTileB];
 #pragma unroll
-  for (int bb = 0; bb < kBatch; ++bb)
+  for (int jj = 0; jj < kTileJ; ++jj)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) a0[bb][e] = a1[bb][e] = 0;
+    for (int x = 0; x < 2 * kTileB; ++x) a[jj][x] = 0;
   uint32_t i = 0;
   while (i < n1) {
     const uint32_t stop = min(n1, i + 15);
     for (; i < stop; ++i) {
-      const v4u pv = ld4(prow + static_cast<size_t>(i) * ln);
+      uint32_t xv[2 * kTileB], pv[kTileJ];
 #pragma unroll
-      for (int bb = 0; bb < kBatch; ++bb) {
-        if (static_cast<uint32_t>(bb) < nb) {
-          const uint32_t* x = baby + (static_cast<size_t>(b0 + bb) * n1 + i) * ctw + static_cast<size_t>(l) * n + k;
-          const v4u x0 = ld4(x), x1 = ld4(x + ln);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            a0[bb][e] += static_cast<uint64_t>(pv[e]) * x0[e];
-            a1[bb][e] += static_cast<uint64_t>(pv[e]) * x1[e];
-          }
-        }
+      for (int bb = 0; bb < kTileB; ++bb) {
+        const uint32_t* xp = xrow + bb * xb_stride + static_cast<size_t>(i) * ctw;
+        xv[2 * bb] = static_cast<uint32_t>(bb) < bn ? xp[0] : 0;
+        xv[2 * bb + 1] = static_cast<uint32_t>(bb) < bn ? xp[ln] : 0;
       }
+#pragma unroll
+      for (int jj = 0; jj < kTileJ; ++jj)
+        pv[jj] = static_cast<uint32_t>(jj) < jn ? prow[jj * pj_stride + static_cast<size_t>(i) * ln] : 0;
+#pragma unroll
+      for (int jj = 0; jj < kTileJ; ++jj)
+#pragma unroll
+        for (int x = 0; x < 2 * kTileB; ++x) a[jj][x] += static_cast<uint64_t>(pv[jj]) * xv[x];
     }
 #pragma unroll
-    for (int bb = 0; bb < kBatch; ++bb)
+    for (int jj = 0; jj < kTileJ; ++jj)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        a0[bb][e] = reduce_u64(a0[bb][e], q, qr);
-        a1[bb][e] = reduce_u64(a1[bb][e], q, qr);
-      }
+      for (int x = 0; x < 2 * kTileB; ++x) a[jj][x] = reduce_u64(a[jj][x], q, qr);
   }
 #pragma unroll
-  for (int bb = 0; bb < kBatch; ++bb) {
-    if (static_cast<uint32_t>(bb) < nb) {
-      uint32_t* o = inner + (static_cast<size_t>(b0 + bb) * n2 + j) * ctw + static_cast<size_t>(l) * n + k;
-      st4(o, v4u{static_cast<uint32_t>(a0[bb][0]), static_cast<uint32_t>(a0[bb][1]), static_cast<uint32_t>(a0[bb][2]),
-                 static_cast<uint32_t>(a0[bb][3])});
-      st4(o + ln, v4u{static_cast<uint32_t>(a1[bb][0]), static_cast<uint32_t>(a1[bb][1]),
-                      static_cast<uint32_t>(a1[bb][2]), static_cast<uint32_t>(a1[bb][3])});
+  for (int bb = 0; bb < kTileB; ++bb) {
+    if (static_cast<uint32_t>(bb) >= bn) continue;
+    uint32_t* o = inner + (static_cast<size_t>(b0 + bb) * n2 + j0) * ctw + static_cast<size_t>(l) * n + c;
+#pragma unroll
+    for (int jj = 0; jj < kTileJ; ++jj) {
+      if (static_cast<uint32_t>(jj) >= jn) continue;
+      o[jj * ctw] = static_cast<uint32_t>(a[jj][2 * bb]);
+      o[jj * ctw + ln] = static_cast<uint32_t>(a[jj][2 * bb + 1]);
     }
   }
 }
@@ -786,13 +797,14 @@ hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, 
                             Seq{n1 - 1, n1, 1}, s);
     if (err != hipSuccess) return err;
   }
-  // inner sums: the full-polynomial MAC (one input), or the batched form that
-  // streams the plaintexts once for every kBatch inputs
+  // inner sums: the full-polynomial MAC (one input), or the register-tiled
+  // batched form
   if (count == 1) {
     err = launch_mac_poly(t, pt, baby, inner, n2, n1, L, s);
   } else {
-    const size_t grid = static_cast<size_t>(L) * (n / (kThreads * 4)) * n2 * ((count + kBatch - 1) / kBatch);
-    bsgs_mac_batch_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, s>>>(t, pt, baby, count, n1, n2, L, inner);
+    const size_t grid = static_cast<size_t>(L) * (n / kThreads) * ((n2 + kTileJ - 1) / kTileJ) *
+                        ((count + kTileB - 1) / kTileB);
+    bsgs_mac_tile_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, s>>>(t, pt, baby, count, n1, n2, L, inner);
     err = hipGetLastError();
   }
   if (err != hipSuccess) return err;
