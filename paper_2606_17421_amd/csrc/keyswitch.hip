@@ -53,6 +53,29 @@ __device__ __forceinline__ uint32_t perm_src(uint32_t i, uint32_t g, uint32_t lo
   return __builtin_bitreverse32(v) >> shift;
 }
 
+// Four consecutive outputs c .. c+3 (c a multiple of 4) read from one aligned
+// quad of the source row: their indices' low two bits are the top two of
+// u = brv(c + e), and u g + (g-1)/2 mod N keeps the low log N - 2 bits of u
+// fixed, so the sources share all bits above the low two.  A thread loads the
+// quad once (16 bytes) and selects within it, instead of four scattered words.
+struct QuadSrc {
+  uint32_t base;   // the quad's first index
+  uint32_t sel[4];
+};
+__device__ __forceinline__ QuadSrc quad_src(uint32_t c, uint32_t g, uint32_t log_n) {
+  QuadSrc x;
+  uint32_t s[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) s[e] = perm_src(c + e, g, log_n);
+  x.base = s[0] & ~3u;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x.sel[e] = s[e] & 3u;
+  return x;
+}
+__device__ __forceinline__ uint32_t pick(const v4u& v, uint32_t k) {
+  return k == 0 ? v[0] : k == 1 ? v[1] : k == 2 ? v[2] : v[3];
+}
+
 // A sequence of ciphertexts [2][L][N] in memory: element m sits at ciphertext
 // position (m / grp) * grp_stride + off + m % grp from the base.
 struct Seq {
@@ -246,6 +269,10 @@ __global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPe
 // cache by the same thread.  When keys x primes x N/4 threads are too few to
 // fill the chip (small rings, large batches), the loop over u is cut into
 // `chunks` ranges on as many workgroups (blockIdx.x / blocks_per_chunk).
+// With KL = L > 0 (L <= 4) the thread's 8 L key words stay in registers for
+// the whole loop instead of being re-read per use (past L2 once the keys of
+// a rotation set outgrow it); KL = 0 takes any L.
+template <int KL>
 __global__ __launch_bounds__(kThreads) void ks_inner_kernel(Tables tb, const uint32_t* __restrict__ D,
                                                             const uint32_t* __restrict__ ksk, uint32_t L,
                                                             uint32_t rotations, RotPlan plan,
@@ -260,9 +287,7 @@ __global__ __launch_bounds__(kThreads) void ks_inner_kernel(Tables tb, const uin
   const uint32_t slot = static_cast<uint32_t>(row / Lp), j = static_cast<uint32_t>(row % Lp);
   const uint32_t c = static_cast<uint32_t>(i & (n - 1));
   const RotIndex x0 = rot_index(slot, plan, log_n);        // the element depends on the slot only
-  uint32_t src[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) src[e] = perm_src(c + e, x0.g, log_n);
+  const QuadSrc qs = quad_src(c, x0.g, log_n);
   const size_t key_stride = static_cast<size_t>(2) * Lp * n;        // one digit of one key
   const uint32_t* key = ksk + static_cast<size_t>(slot) * L * key_stride + static_cast<size_t>(j) * n + c;
   const uint32_t pj = tb.q[j];
@@ -270,20 +295,34 @@ __global__ __launch_bounds__(kThreads) void ks_inner_kernel(Tables tb, const uin
   const uint32_t uses = rotations / plan.key_period;        // rotations per key
   const uint32_t u_begin = static_cast<uint32_t>(static_cast<uint64_t>(uses) * chunk / chunks);
   const uint32_t u_end = static_cast<uint32_t>(static_cast<uint64_t>(uses) * (chunk + 1) / chunks);
+  constexpr int KR = KL > 0 ? KL : 1;
+  v4u kr0[KR], kr1[KR];
+  if constexpr (KL > 0) {
+#pragma unroll
+    for (int d = 0; d < KL; ++d) {
+      kr0[d] = ld4(key + d * key_stride);
+      kr1[d] = ld4(key + d * key_stride + static_cast<size_t>(Lp) * n);
+    }
+  }
   for (uint32_t k = slot + u_begin * plan.key_period; k < u_end * plan.key_period; k += plan.key_period) {
     const uint32_t m = k / plan.per_input;
     const uint32_t* dig = D + (static_cast<size_t>(m) * L * Lp + j) * n;
     uint64_t a0[4] = {0, 0, 0, 0}, a1[4] = {0, 0, 0, 0};
-    for (uint32_t d = 0; d < L; ++d) {
-      const uint32_t* drow = dig + static_cast<size_t>(d) * Lp * n;
-      const v4u k0 = ld4(key + d * key_stride);
-      const v4u k1 = ld4(key + d * key_stride + static_cast<size_t>(Lp) * n);
+    auto digit = [&](uint32_t d, const v4u& k0, const v4u& k1) {
+      const v4u dq = ld4(dig + static_cast<size_t>(d) * Lp * n + qs.base);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const uint64_t dv = drow[src[e]];
+        const uint64_t dv = pick(dq, qs.sel[e]);
         a0[e] += dv * k0[e];
         a1[e] += dv * k1[e];
       }
+    };
+    if constexpr (KL > 0) {
+#pragma unroll
+      for (int d = 0; d < KL; ++d) digit(d, kr0[d], kr1[d]);
+    } else {
+      for (uint32_t d = 0; d < L; ++d)
+        digit(d, ld4(key + d * key_stride), ld4(key + d * key_stride + static_cast<size_t>(Lp) * n));
     }
     v4u o0, o1;
 #pragma unroll
@@ -315,9 +354,11 @@ __global__ __launch_bounds__(kThreads) void rot_combine_kernel(Tables tb, const 
   const v4u u0 = ld4(tmp + base);
   const v4u u1 = ld4(tmp + base + static_cast<size_t>(L) * n);
   const uint32_t q = tb.q[l];
+  const QuadSrc qs = quad_src(c, x.g, log_n);
+  const v4u cq = ld4(c0 + qs.base);
   v4u o;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) o[e] = add_mod(c0[perm_src(c + e, x.g, log_n)], u0[e], q);
+  for (int e = 0; e < 4; ++e) o[e] = add_mod(pick(cq, qs.sel[e]), u0[e], q);
   uint32_t* dst = out + seq_pos(k, out_seq) * ctw + static_cast<size_t>(l) * n + c;
   st4(dst, o);
   st4(dst + static_cast<size_t>(L) * n, u1);
@@ -705,7 +746,13 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
     const uint32_t uses = rotations / plan.key_period;
     const uint32_t want = (4 * t.num_cus + blocks - 1) / blocks;
     const uint32_t chunks = want < 1 ? 1 : (want > uses ? uses : want);
-    ks_inner_kernel<<<blocks * chunks, kThreads, 0, s>>>(t, w.D, ksk, L, rotations, plan, blocks, chunks, w.acc);
+    const dim3 g(blocks * chunks);
+    switch (L) {
+      case 2: ks_inner_kernel<2><<<g, kThreads, 0, s>>>(t, w.D, ksk, L, rotations, plan, blocks, chunks, w.acc); break;
+      case 3: ks_inner_kernel<3><<<g, kThreads, 0, s>>>(t, w.D, ksk, L, rotations, plan, blocks, chunks, w.acc); break;
+      case 4: ks_inner_kernel<4><<<g, kThreads, 0, s>>>(t, w.D, ksk, L, rotations, plan, blocks, chunks, w.acc); break;
+      default: ks_inner_kernel<0><<<g, kThreads, 0, s>>>(t, w.D, ksk, L, rotations, plan, blocks, chunks, w.acc); break;
+    }
   }
   if ((err = hipGetLastError()) != hipSuccess || out == nullptr) return err;
   if (t.log_n <= 14 && 4 * static_cast<size_t>(rotations) <= t.num_cus) {

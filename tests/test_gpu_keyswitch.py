@@ -80,11 +80,14 @@ def test_keygen_rotation_bit_exact(gpu_lib, log_n, L, r0, r_step, count):
                                                    (12, 3, True, (4, 8)), (13, 2, True, (1, 2, 3)),
                                                    (14, 3, False, (2, 6)), (16, 2, False, (1,)),
                                                    (10, 2, True, (511,)),                  # a left rotation by N/2 - 1 = right by 1
-                                                   (14, 3, False, tuple(range(1, 23)))])   # 264 ModUp groups: two-launch form
+                                                   (14, 3, False, tuple(range(1, 23))),    # 264 ModUp groups: two-launch form
+                                                   (10, 5, True, (1, 2))])                 # 5 digits: keys re-read per use
 def test_rotate_bit_exact(gpu_lib, log_n, L, hoisted, steps):
     """Bit-exact against the oracle.  The ModUp runs fused while its (input, digit, prime)
     workgroups number at most one per CU (256), else in two launches (22 inputs x 3 digits
-    x 4 primes at 2^14), and at 2^16 as the four-launch pass route."""
+    x 4 primes at 2^14), and at 2^16 as the four-launch pass route.  The key-switching
+    inner product holds the keys in registers for 2 to 4 digits, and re-reads them for
+    more (5 here)."""
     ck = gpu_lib
     ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 740 + log_n + L)
     count = len(steps)
