@@ -12,12 +12,14 @@
 //
 // Key switching (hybrid, one digit per limb): the digits of c1 are the centred
 // coefficient vectors of its limbs, lifted to every prime of q_0..q_{L-1}, P
-// (ModUp: batched INTT, a lift pass, batched NTT).  A rotation then needs
-// only its key and an index permutation: sigma_g commutes with the digit
-// decomposition exactly (the centred lift is odd-symmetric for odd q), so the
-// inner product reads the unrotated digits through the permutation.  All
-// rotations of one ciphertext share one ModUp (hoisting).  The division by P
-// (ModDown) is the rescale that drops the last prime.
+// (ModUp: an INTT per digit, then a lifted NTT per digit and prime, in one,
+// two or four launches by size).  A rotation then needs only its key and an
+// index permutation: sigma_g commutes with the digit decomposition exactly
+// (the centred lift is odd-symmetric for odd q), so the inner product reads
+// the unrotated digits through the permutation.  All rotations of one
+// ciphertext share one ModUp (hoisting).  The division by P (ModDown) is the
+// rescale that drops the last prime, fused with the rotation's combine up to
+// 2^14; the BSGS giant steps sum their inner products first and divide once.
 #include "ntt_core.hpp"
 
 namespace ckks {
@@ -336,7 +338,8 @@ __global__ __launch_bounds__(kThreads) void ks_inner_kernel(Tables tb, const uin
   }
 }
 
-// Rotation k's result: out[k] = (sigma_g(c0_m) + u0, u1), u = ModDown(acc[k]) (tmp[k][2][L][N]).
+// Rotation k's result: out[k] = (sigma_g(c0_m) + u0, u1), u = ModDown(acc[k]) (tmp[k][2][L][N]);
+// at 2^15 and 2^16, after the separate ModDown.
 __global__ __launch_bounds__(kThreads) void rot_combine_kernel(Tables tb, const uint32_t* __restrict__ ct, Seq in_seq,
                                                                const uint32_t* __restrict__ tmp, uint32_t L,
                                                                uint32_t rotations, RotPlan plan,
@@ -621,7 +624,8 @@ __global__ __launch_bounds__(kThreads) void bsgs_mac_tile_kernel(Tables tb, cons
 }
 
 // Workspace of rotate(): T [inputs][L][N], D [inputs][L][L+1][N],
-// acc [rotations][2][L+1][N], tmp [rotations][2][L][N], rescale scratch.
+// acc [rotations][2][L+1][N], tmp [rotations][2][L][N] (the separate ModDown's
+// output, 2^15 and 2^16), rescale scratch.
 struct RotWs {
   uint32_t *T, *D, *acc, *tmp;
   void* rs;
