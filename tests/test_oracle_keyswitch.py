@@ -123,6 +123,35 @@ def test_keyswitch_decrypts_to_c_times_s_from(log_n, L):
     assert err > 0                                           # the key's error is really there
 
 
+@pytest.mark.parametrize("log_n,L", [(6, 2), (8, 3)])
+def test_keyswitch_ext_decrypts_to_p_times_c_times_s_from(log_n, L):
+    """Before the division by P: a0 + a1 s_to = P c s_from + sum_i d_i e_i over all L + 1
+    primes, |d_i| <= q_i / 2 and |e_i| <= 19 per coefficient, so the CRT-lifted difference
+    stays within sum_i N (q_i/2) 19 (the same bound as after the division, times P)."""
+    n, qs_p, psis_p, s, st = _chain(log_n, L, 50 + log_n)
+    s2 = gen.ternary_secret(st["secret"], n)
+    ksk = _key(st, s2, s, qs_p, psis_p, log_n)
+    c = gen.uniform_residues(st["residues"], (), qs_p[:L], n)
+    ext = KS.keyswitch_ext(c, ksk, qs_p, psis_p, log_n)
+    assert ext.shape == (2, L + 1, n)
+    P = qs_p[-1]
+    got, want = [], []
+    c_int = _centred_lift(np.stack([intt(c[l].astype(np.uint64), qs_p[l], psis_p[l], log_n) for l in range(L)]),
+                          qs_p[:L])                                 # c as centred integers
+    for l in range(L + 1):
+        q, ps = qs_p[l], psis_p[l]
+        qq = np.uint64(q)
+        s_hat = ntt(np.mod(s, q).astype(np.uint64), q, ps, log_n)
+        s2_hat = ntt(np.mod(s2, q).astype(np.uint64), q, ps, log_n)
+        c_hat = ntt(np.array([int(x) % q for x in c_int], dtype=np.uint64), q, ps, log_n)
+        got.append(intt((ext[0, l] + (ext[1, l] * s_hat) % qq) % qq, q, ps, log_n))
+        want.append(intt((((c_hat * s2_hat) % qq) * np.uint64(P % q)) % qq, q, ps, log_n))
+    diff = _centred_lift(np.stack(got), qs_p) - _centred_lift(np.stack(want), qs_p)
+    err = max(abs(int(x)) for x in diff)
+    assert err <= sum(n * (q // 2) * 19 for q in qs_p[:-1])
+    assert err > n * 19                                       # the digits' error terms are really there
+
+
 def test_keyswitch_with_a_wrong_key_fails_the_bound():
     """A key for a different s_from gives an error of the order of Q, far past the bound."""
     log_n, L = 6, 2
