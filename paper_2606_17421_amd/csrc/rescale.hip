@@ -92,84 +92,102 @@ __global__ __launch_bounds__((WholePlan<LOGN, kSplit>::P::T), (WholePlan<LOGN, k
 //   = (c_l q_t^-1 - NTT_l(r1 q_t^-1 + r2)) q_u^-1     mod q_l,
 // the same residues as the two rescales in turn.  For launches of few
 // polynomials (the key-switched sum of the BSGS giant steps: its division by
-// the special prime, then the product's own rescale): one workgroup per output
-// limb of one polynomial (blockIdx.y = l), three transforms in its chain
-// instead of four over two launches, no intermediate rows.  (A loop over the
-// limbs would hold r1, r2 and the row in registers at once and spill.)
+// the special prime, then the product's own rescale), in two launches whose
+// chains are one transform each:
+//   rescale2_inv_kernel, one workgroup per polynomial and row (t or u): the
+//     inverse transform of that row, r1 (centred) or INTT_u(c_u) stored to the
+//     workspace in the plan's register order (element e of thread t at
+//     e * T + t, coalesced both ways, read back by the same plan's threads);
+//   rescale2_fwd_kernel, one workgroup per polynomial and output limb l: r2
+//     from the two stored rows, then NTT_l(r1 q_t^-1 + r2) and the combine.
+// (One launch doing all three transforms per workgroup took 20.5 us for one
+// ciphertext at 2^13; a loop over the limbs would also hold r1, r2 and the row
+// in registers at once and spill.)
 template <int LOGN>
-__global__ __launch_bounds__((WholePlan<LOGN, true>::P::T), (WholePlan<LOGN, true>::kWavesPerSimd)) void rescale2_kernel(
-    Tables tb, const uint32_t* __restrict__ in, uint32_t* __restrict__ out, uint32_t limbs) {
+__global__ __launch_bounds__((WholePlan<LOGN, true>::P::T), (WholePlan<LOGN, true>::kWavesPerSimd)) void
+rescale2_inv_kernel(Tables tb, const uint32_t* __restrict__ in, uint32_t limbs, uint32_t* __restrict__ ws) {
   using P = typename WholePlan<LOGN, true>::P;
   constexpr int LOGE = WholePlan<LOGN, true>::LOGE;
   constexpr int N = P::B;
   constexpr bool kCoalesce = LOGN <= 14;
   __shared__ uint32_t lds[P::lds_words];
-  const size_t poly = blockIdx.x;  // ciphertext * 2 + component
+  const size_t poly = blockIdx.x;                     // ciphertext * 2 + component
+  const uint32_t which = blockIdx.y;                  // 0: row t (r1), 1: row u
+  const uint32_t m = limbs - 1 - which;
+  const uint32_t t = threadIdx.x;
+  const uint32_t* src = in + (poly * limbs + m) * N;
+  uint32_t v[P::E];
+  if constexpr (kCoalesce) {
+    const uint32_t* sm = src + pos_coalesced<LOGE>(t, 0);
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = sm[j << 6];
+    wave_relayout<LOGN, LOGE, true>(v, t, lds);
+  } else {
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) v[j] = src[P::template pos<P::NG - 1>(t, j)];
+  }
+  const size_t tm = static_cast<size_t>(m) << LOGN;
+  const uint32_t qm = tb.q[m];
+  inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + tm, tb.inv_shoup + tm, qm, lds);
+  const uint32_t ni = tb.ninv[m], nis = tb.ninv_shoup[m];
+  uint32_t* dst = ws + (poly * 2 + which) * N + t;
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) {
+    const uint32_t x = mul_shoup(v[j], ni, nis, qm);
+    // row t: the centred value as a two's-complement word; row u: the residue
+    dst[j * P::T] = which == 0 && x > (qm >> 1) ? x - qm : x;
+  }
+}
+
+template <int LOGN>
+__global__ __launch_bounds__((WholePlan<LOGN, true>::P::T), (WholePlan<LOGN, true>::kWavesPerSimd)) void
+rescale2_fwd_kernel(Tables tb, const uint32_t* __restrict__ in, const uint32_t* __restrict__ ws, uint32_t limbs,
+                    uint32_t* __restrict__ out) {
+  using P = typename WholePlan<LOGN, true>::P;
+  constexpr int LOGE = WholePlan<LOGN, true>::LOGE;
+  constexpr int N = P::B;
+  constexpr bool kCoalesce = LOGN <= 14;
+  __shared__ uint32_t lds[P::lds_words];
+  const size_t poly = blockIdx.x;
   const uint32_t t = threadIdx.x;
   const uint32_t* src = in + poly * limbs * N;
   uint32_t* dst = out + poly * (limbs - 2) * N;
   const uint32_t top = limbs - 1, mid = limbs - 2;
-
-  // coefficients of limb m of this polynomial (times N^-1), group-0 layout
-  auto inverse_row = [&](uint32_t m, uint32_t (&v)[P::E]) {
-    if constexpr (kCoalesce) {
-      const uint32_t* sm = src + static_cast<size_t>(m) * N + pos_coalesced<LOGE>(t, 0);
-#pragma unroll
-      for (int j = 0; j < P::E; ++j) v[j] = sm[j << 6];
-      wave_relayout<LOGN, LOGE, true>(v, t, lds);
-    } else {
-#pragma unroll
-      for (int j = 0; j < P::E; ++j) v[j] = src[static_cast<size_t>(m) * N + P::template pos<P::NG - 1>(t, j)];
-    }
-    const size_t tm = static_cast<size_t>(m) << LOGN;
-    const uint32_t qm = tb.q[m];
-    inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + tm, tb.inv_shoup + tm, qm, lds);
-    const uint32_t ni = tb.ninv[m], nis = tb.ninv_shoup[m];
-#pragma unroll
-    for (int j = 0; j < P::E; ++j) v[j] = mul_shoup(v[j], ni, nis, qm);
-  };
-  auto centred = [](uint32_t x, uint32_t q) {
-    return x > (q >> 1) ? static_cast<int32_t>(x) - static_cast<int32_t>(q) : static_cast<int32_t>(x);
-  };
   auto lift = [](int32_t r, uint32_t q) {   // |r| < 2^29 < q
     return static_cast<uint32_t>(r < 0 ? r + static_cast<int32_t>(q) : r);
   };
-
-  uint32_t v[P::E];
+  const uint32_t* w1 = ws + (poly * 2) * N + t;
+  const uint32_t* w2 = w1 + N;
   int32_t r1[P::E], r2[P::E];
-  inverse_row(top, v);
-  const uint32_t qt = tb.q[top];
-#pragma unroll
-  for (int j = 0; j < P::E; ++j) r1[j] = centred(v[j], qt);
-  __syncthreads();  // every wave's reads of the first transform's last exchange are done
-  inverse_row(mid, v);
   {
     const uint32_t qu = tb.q[mid];
     const uint32_t ti = tb.qinv[top * tb.L + mid], tis = tb.qinv_shoup[top * tb.L + mid];
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) r2[j] = centred(mul_shoup(sub_mod(v[j], lift(r1[j], qu), qu), ti, tis, qu), qu);
+    for (int j = 0; j < P::E; ++j) {
+      r1[j] = static_cast<int32_t>(w1[j * P::T]);
+      const uint32_t x = mul_shoup(sub_mod(w2[j * P::T], lift(r1[j], qu), qu), ti, tis, qu);
+      r2[j] = x > (qu >> 1) ? static_cast<int32_t>(x) - static_cast<int32_t>(qu) : static_cast<int32_t>(x);
+    }
   }
-
-  {
-    const uint32_t l = blockIdx.y, q = tb.q[l];
-    const uint32_t ti = tb.qinv[top * tb.L + l], tis = tb.qinv_shoup[top * tb.L + l];
-    const uint32_t ui = tb.qinv[mid * tb.L + l], uis = tb.qinv_shoup[mid * tb.L + l];
+  const uint32_t l = blockIdx.y, q = tb.q[l];
+  const uint32_t ti = tb.qinv[top * tb.L + l], tis = tb.qinv_shoup[top * tb.L + l];
+  const uint32_t ui = tb.qinv[mid * tb.L + l], uis = tb.qinv_shoup[mid * tb.L + l];
+  uint32_t v[P::E];
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) v[j] = add_mod(mul_shoup(lift(r1[j], q), ti, tis, q), lift(r2[j], q), q);
-    const size_t tl = static_cast<size_t>(l) << LOGN;
-    fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
-    if constexpr (kCoalesce) {
-      wave_relayout<LOGN, LOGE, false>(v, t, lds);
-      const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
-      uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
+  for (int j = 0; j < P::E; ++j) v[j] = add_mod(mul_shoup(lift(r1[j], q), ti, tis, q), lift(r2[j], q), q);
+  const size_t tl = static_cast<size_t>(l) << LOGN;
+  fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+  if constexpr (kCoalesce) {
+    wave_relayout<LOGN, LOGE, false>(v, t, lds);
+    const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
+    uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-      for (int j = 0; j < P::E; ++j) dl[j << 6] = mul_shoup(sub_mod(mul_shoup(sl[j << 6], ti, tis, q), v[j], q), ui, uis, q);
-    } else {
+    for (int j = 0; j < P::E; ++j) dl[j << 6] = mul_shoup(sub_mod(mul_shoup(sl[j << 6], ti, tis, q), v[j], q), ui, uis, q);
+  } else {
 #pragma unroll
-      for (int j = 0; j < P::E; ++j) {
-        const size_t x = static_cast<size_t>(l) * N + P::template pos<P::NG - 1>(t, j);
-        dst[x] = mul_shoup(sub_mod(mul_shoup(src[x], ti, tis, q), v[j], q), ui, uis, q);
-      }
+    for (int j = 0; j < P::E; ++j) {
+      const size_t x = static_cast<size_t>(l) * N + P::template pos<P::NG - 1>(t, j);
+      dst[x] = mul_shoup(sub_mod(mul_shoup(src[x], ti, tis, q), v[j], q), ui, uis, q);
     }
   }
 }
@@ -336,22 +354,29 @@ hipError_t launch_rescale(const Tables& t, const uint32_t* ct_in, uint32_t* ct_o
   }
 }
 
-// Two rescales in turn (limbs -> limbs - 2): one launch of rescale2_kernel for
-// fewer than num_cus / 4 ciphertexts up to 2^15, else the two rescales with
-// the intermediate [count][2][limbs-1][N] in `mid` (caller-provided).
+// Two rescales in turn (limbs -> limbs - 2): rescale2_inv_kernel then
+// rescale2_fwd_kernel for fewer than num_cus / 4 ciphertexts up to 2^15 (their
+// 4 count N words of rows in `mid`), else the two rescales with the
+// intermediate [count][2][limbs-1][N] in `mid`.  `mid` is caller-provided.
 hipError_t launch_rescale2(const Tables& t, const uint32_t* ct_in, uint32_t* mid, uint32_t* ct_out, uint32_t count,
                            uint32_t limbs, void* workspace, hipStream_t s) {
   if (count == 0) return hipSuccess;
   if (limbs < 3) return hipErrorInvalidValue;
   if (t.log_n <= 15 && 4 * static_cast<size_t>(count) <= t.num_cus) {
-    const dim3 grid(2 * count, limbs - 2);
+    const dim3 gi(2 * count, 2), gf(2 * count, limbs - 2);
     switch (t.log_n) {
-      case 10: rescale2_kernel<10><<<grid, WholePlan<10, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
-      case 11: rescale2_kernel<11><<<grid, WholePlan<11, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
-      case 12: rescale2_kernel<12><<<grid, WholePlan<12, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
-      case 13: rescale2_kernel<13><<<grid, WholePlan<13, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
-      case 14: rescale2_kernel<14><<<grid, WholePlan<14, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
-      default: rescale2_kernel<15><<<grid, WholePlan<15, true>::P::T, 0, s>>>(t, ct_in, ct_out, limbs); break;
+#define CKKS_R2(LN)                                                                                     \
+  case LN:                                                                                              \
+    rescale2_inv_kernel<LN><<<gi, WholePlan<LN, true>::P::T, 0, s>>>(t, ct_in, limbs, mid);             \
+    rescale2_fwd_kernel<LN><<<gf, WholePlan<LN, true>::P::T, 0, s>>>(t, ct_in, mid, limbs, ct_out);     \
+    break;
+      CKKS_R2(10)
+      CKKS_R2(11)
+      CKKS_R2(12)
+      CKKS_R2(13)
+      CKKS_R2(14)
+      default: CKKS_R2(15)
+#undef CKKS_R2
     }
     return hipGetLastError();
   }
