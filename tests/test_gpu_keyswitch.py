@@ -108,14 +108,16 @@ def test_rotate_bit_exact(gpu_lib, log_n, L, hoisted, steps):
 @pytest.mark.parametrize("log_n,L,n1,n2,count", [(10, 2, 4, 4, 2), (11, 3, 3, 5, 1), (10, 3, 1, 4, 1),
                                                  (10, 2, 4, 1, 1), (10, 2, 2, 3, 6), (10, 2, 2, 2, 65),
                                                  (15, 2, 2, 2, 1), (16, 2, 2, 2, 1), (11, 3, 2, 10, 3),
-                                                 (12, 3, 8, 17, 5)])
+                                                 (12, 3, 8, 17, 5), (10, 4, 16, 2, 20)])
 def test_bsgs_bit_exact(gpu_lib, log_n, L, n1, n2, count):
     """Any residues: the product is exact modular arithmetic, so uniform plaintexts and
     ciphertexts are compared with the oracle bit for bit.  The closing pair of rescales
     (division by P, then by q_(L-1)) runs as one launch for few inputs up to 2^15 and as
     two rescales for 65 inputs (more than a quarter of 256 CUs) and at 2^16.  Several
     inputs take the register-tiled MAC (8 rows by 2 inputs per thread): n2 = 10 and 17
-    and 3 or 5 inputs leave partial tiles in both directions."""
+    and 3 or 5 inputs leave partial tiles in both directions.  With 20 inputs, n1 = 16 and
+    4 digits at 2^10 the key-switching loop over each baby key's 20 uses is cut into
+    chunks that do not divide it evenly (14 on 256 CUs)."""
     ck = gpu_lib
     ctx, qs_p, psis_p, n, st, s, s_ntt = setup(ck, log_n, L, 760 + n1 * 7 + n2)
     pt = gen.uniform_residues(st["residues"], (n2, n1), qs_p[:L], n)
