@@ -552,7 +552,7 @@ __global__ __launch_bounds__(kThreads) void giant_ext_kernel(Tables tb, const ui
 // 2 kTileB input residues for 2 kTileJ kTileB products, so the plaintexts are
 // read count / kTileB times and the inputs n2 / kTileJ times (the previous
 // form, one row by four inputs, re-read every input n2 times and was bound by
-// that L2 traffic).  64-bit sums, reduced every 15 products.  Workgroups that
+// that L2 traffic).  64-bit sums, folded every 11 products.  Workgroups that
 // share a plaintext tile (consecutive b tiles) or an input tile are numbered
 // together and placed on one XCD.
 constexpr int kTileJ = 8, kTileB = 2;
@@ -578,38 +578,58 @@ __global__ __launch_bounds__(kThreads) void bsgs_mac_tile_kernel(Tables tb, cons
   const uint32_t q = tb.q[l];
   const double qr = tb.q_recip[l];
   const size_t ln = static_cast<size_t>(L) * n, ctw = 2 * ln;
-  const uint32_t* prow = pt + (static_cast<size_t>(j0) * n1 * L + l) * n + c;       // + (jj n1 + i) L N
-  const uint32_t* xrow = baby + static_cast<size_t>(b0) * n1 * ctw + static_cast<size_t>(l) * n + c;   // + (bb n1 + i) ctw
+  // row pointers are workgroup-uniform (scalar); the lane adds its coefficient c
+  const uint32_t* prow = pt + (static_cast<size_t>(j0) * n1 * L + l) * n;         // + (jj n1 + i) L N
+  const uint32_t* xrow = baby + static_cast<size_t>(b0) * n1 * ctw + static_cast<size_t>(l) * n;   // + (bb n1 + i) ctw
   const size_t pj_stride = static_cast<size_t>(n1) * ln, xb_stride = static_cast<size_t>(n1) * ctw;
+  // Sums are folded every kFold products: a = hi 2^32 + lo -> hi (2^32 mod q) + lo
+  // (exact mod q) is below 2^62 + 2^32, and kFold = 11 further products below
+  // 2^60 keep it below 2^64; one full reduction at the end.
+  constexpr uint32_t kFold = 11;
+  const uint32_t c32 = reduce_u64(uint64_t{1} << 32, q, qr);
   uint64_t a[kTileJ][2 * kTileB];
 #pragma unroll
   for (int jj = 0; jj < kTileJ; ++jj)
 #pragma unroll
     for (int x = 0; x < 2 * kTileB; ++x) a[jj][x] = 0;
-  uint32_t i = 0;
-  while (i < n1) {
-    const uint32_t stop = min(n1, i + 15);
-    for (; i < stop; ++i) {
-      uint32_t xv[2 * kTileB], pv[kTileJ];
+  uint32_t since = 0;
+  for (uint32_t i = 0; i < n1; ++i) {
+    // every load is issued (rows past a partial tile read the tile's first
+    // row, in bounds) and its value zeroed by a select, so the 12 loads go
+    // out back to back instead of one branch each
+    uint32_t xv[2 * kTileB], pv[kTileJ];
 #pragma unroll
-      for (int bb = 0; bb < kTileB; ++bb) {
-        const uint32_t* xp = xrow + bb * xb_stride + static_cast<size_t>(i) * ctw;
-        xv[2 * bb] = static_cast<uint32_t>(bb) < bn ? xp[0] : 0;
-        xv[2 * bb + 1] = static_cast<uint32_t>(bb) < bn ? xp[ln] : 0;
-      }
+    for (int bb = 0; bb < kTileB; ++bb) {
+      const bool in = static_cast<uint32_t>(bb) < bn;
+      const uint32_t* xp = xrow + (in ? bb : 0) * xb_stride + static_cast<size_t>(i) * ctw;
+      const uint32_t x0 = xp[c], x1 = (xp + ln)[c];
+      xv[2 * bb] = in ? x0 : 0;
+      xv[2 * bb + 1] = in ? x1 : 0;
+    }
 #pragma unroll
-      for (int jj = 0; jj < kTileJ; ++jj)
-        pv[jj] = static_cast<uint32_t>(jj) < jn ? prow[jj * pj_stride + static_cast<size_t>(i) * ln] : 0;
-#pragma unroll
-      for (int jj = 0; jj < kTileJ; ++jj)
-#pragma unroll
-        for (int x = 0; x < 2 * kTileB; ++x) a[jj][x] += static_cast<uint64_t>(pv[jj]) * xv[x];
+    for (int jj = 0; jj < kTileJ; ++jj) {
+      const bool in = static_cast<uint32_t>(jj) < jn;
+      const uint32_t p = (prow + (in ? jj : 0) * pj_stride + static_cast<size_t>(i) * ln)[c];
+      pv[jj] = in ? p : 0;
     }
 #pragma unroll
     for (int jj = 0; jj < kTileJ; ++jj)
 #pragma unroll
-      for (int x = 0; x < 2 * kTileB; ++x) a[jj][x] = reduce_u64(a[jj][x], q, qr);
+      for (int x = 0; x < 2 * kTileB; ++x) a[jj][x] += static_cast<uint64_t>(pv[jj]) * xv[x];
+    if (++since == kFold) {
+      since = 0;
+#pragma unroll
+      for (int jj = 0; jj < kTileJ; ++jj)
+#pragma unroll
+        for (int x = 0; x < 2 * kTileB; ++x)
+          a[jj][x] = static_cast<uint64_t>(static_cast<uint32_t>(a[jj][x] >> 32)) * c32 +
+                     static_cast<uint32_t>(a[jj][x]);
+    }
   }
+#pragma unroll
+  for (int jj = 0; jj < kTileJ; ++jj)
+#pragma unroll
+    for (int x = 0; x < 2 * kTileB; ++x) a[jj][x] = reduce_u64(a[jj][x], q, qr);
 #pragma unroll
   for (int bb = 0; bb < kTileB; ++bb) {
     if (static_cast<uint32_t>(bb) >= bn) continue;
