@@ -525,11 +525,17 @@ __global__ __launch_bounds__(kThreads) void giant_ext_kernel(Tables tb, const ui
   for (int e = 0; e < 4; ++e) g4 = (g4 * g1) & mask;       // g1^4
   uint32_t sy = (w == 0 && l < L) ? in_b[(static_cast<size_t>(p) * L + l) * n + c] : 0;
   uint32_t sa = 0;
+  // the row kind is workgroup-uniform: one loop per kind, no branch inside
+  if (carries_sigma) {
 #pragma unroll 4
-  for (uint32_t j = 1 + w; j < n2; j += 4) {
-    sa = add_mod(sa, acc_b[(j - 1) * extw], q);
-    if (carries_sigma) sy = add_mod(sy, in_b[j * ctw + static_cast<size_t>(l) * n + perm_src(c, g, log_n)], q);
-    g = (g * g4) & mask;
+    for (uint32_t j = 1 + w; j < n2; j += 4) {
+      sa = add_mod(sa, acc_b[(j - 1) * extw], q);
+      sy = add_mod(sy, in_b[j * ctw + static_cast<size_t>(l) * n + perm_src(c, g, log_n)], q);
+      g = (g * g4) & mask;
+    }
+  } else {
+#pragma unroll 4
+    for (uint32_t j = 1 + w; j < n2; j += 4) sa = add_mod(sa, acc_b[(j - 1) * extw], q);
   }
   if (w > 0) {
     part[0][w - 1][lane] = sy;
