@@ -383,16 +383,29 @@ __global__ __launch_bounds__(kThreads) void rot_combine_kernel(Tables tb, const 
 template <int LOGN>
 __global__ __launch_bounds__((WholePlan<LOGN, true>::P::T), (WholePlan<LOGN, true>::kWavesPerSimd)) void
 moddown_combine_kernel(Tables tb, const uint32_t* __restrict__ acc, const uint32_t* __restrict__ ct, Seq in_seq,
-                       uint32_t L, RotPlan plan, uint32_t* __restrict__ out, Seq out_seq) {
+                       uint32_t L, uint32_t rotations, RotPlan plan, uint32_t* __restrict__ out, Seq out_seq,
+                       Seq copy_seq) {
   using P = typename WholePlan<LOGN, true>::P;
   constexpr int LOGE = WholePlan<LOGN, true>::LOGE;
   constexpr int N = P::B;
   __shared__ uint32_t lds[P::lds_words];
+  const uint32_t t = threadIdx.x;
+  const uint32_t c_base = pos_coalesced<LOGE>(t, 0);
+  if (blockIdx.x >= 2 * rotations) {
+    // workgroups past the rotations copy limb blockIdx.y of component p of
+    // input m unchanged to element m of copy_seq (the BSGS baby slot 0), so
+    // that copy needs no launch of its own; the whole workgroup returns here
+    const uint32_t idx = blockIdx.x - 2 * rotations, m = idx >> 1, pc = idx & 1;
+    const size_t row = static_cast<size_t>(pc) * L * N + static_cast<size_t>(blockIdx.y) * N + c_base;
+    const uint32_t* cs = ct + seq_pos(m, in_seq) * 2 * L * N + row;
+    uint32_t* cd = out + seq_pos(m, copy_seq) * 2 * L * N + row;
+#pragma unroll
+    for (int j = 0; j < P::E; ++j) cd[j << 6] = cs[j << 6];
+    return;
+  }
   const uint32_t poly = blockIdx.x;                         // k * 2 + p
   const uint32_t k = poly >> 1, p = poly & 1;
-  const uint32_t t = threadIdx.x;
   const uint32_t top = L;                                   // the special prime's row
-  const uint32_t c_base = pos_coalesced<LOGE>(t, 0);
   const uint32_t* src = acc + static_cast<size_t>(poly) * (L + 1) * N + c_base;
   const RotIndex x = rot_index(k, plan, LOGN);
   const size_t ctw = static_cast<size_t>(2) * L * N;
@@ -725,7 +738,7 @@ hipError_t launch_automorphism(const Tables& t, const uint32_t* in, size_t rows,
 // region (rot_layout(..).acc) for a consumer that sums before dividing by P.
 hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, uint32_t inputs, uint32_t rotations,
                              RotPlan plan, const uint32_t* ksk, void* workspace, uint32_t* out, Seq out_seq,
-                             hipStream_t s) {
+                             hipStream_t s, const Seq* copy_inputs) {
   if (rotations == 0) return hipSuccess;
   if (rotations % plan.key_period != 0) return hipErrorInvalidValue;   // every key serves whole batches
   const uint32_t L = t.L - 1, Lp = L + 1;
@@ -789,12 +802,14 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
   }
   if ((err = hipGetLastError()) != hipSuccess || out == nullptr) return err;
   if (t.log_n <= 14) {
-    const dim3 grid(2 * rotations, L);
+    const uint32_t copies = copy_inputs ? inputs : 0;
+    const Seq cseq = copy_inputs ? *copy_inputs : contiguous();
+    const dim3 grid(2 * (rotations + copies), L);
     switch (t.log_n) {
 #define CKKS_MDC(LN)                                                                                       \
   case LN:                                                                                                 \
-    moddown_combine_kernel<LN><<<grid, WholePlan<LN, true>::P::T, 0, s>>>(t, w.acc, ct, in_seq, L, plan, out, \
-                                                                          out_seq);                        \
+    moddown_combine_kernel<LN><<<grid, WholePlan<LN, true>::P::T, 0, s>>>(t, w.acc, ct, in_seq, L, rotations, \
+                                                                          plan, out, out_seq, cseq);       \
     break;
       CKKS_MDC(10)
       CKKS_MDC(11)
@@ -805,6 +820,7 @@ hipError_t launch_rotate_seq(const Tables& t, const uint32_t* ct, Seq in_seq, ui
     }
     return hipGetLastError();
   }
+  if (copy_inputs != nullptr) return hipErrorInvalidValue;   // the input copy rides on the fused form only
   err = launch_rescale(t, w.acc, w.tmp, rotations, Lp, w.rs, s);
   if (err != hipSuccess) return err;
   rot_combine_kernel<<<grid_for(static_cast<size_t>(rotations) * L * n / 4), kThreads, 0, s>>>(
@@ -851,7 +867,7 @@ hipError_t launch_rotate(const Tables& t, const uint32_t* ct, uint32_t count, ui
   // hoisted: count rotations of one input; else rotation k of input k
   RotPlan plan{hoisted ? count : 1u, count, r0, r_step, galois};
   return launch_rotate_seq(t, ct, contiguous(), hoisted ? 1 : count, count, plan, ksk, workspace, out, contiguous(),
-                           s);
+                           s, nullptr);
 }
 
 // y = sum_j rot( sum_i pt[j][i] (.) rot(x, i), j n1 ), rescaled, for each of
@@ -868,13 +884,19 @@ hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, 
   uint32_t* ext = inner + static_cast<size_t>(count) * n2 * ctw;
   void* rws = ext + static_cast<size_t>(count) * 2 * (L + 1) * n;
   // baby steps: element 0 of each input's group is the input itself, then its
-  // rotations by 1 .. n1-1 (one ModUp per input)
-  hipError_t err = hipMemcpy2DAsync(baby, n1 * ctw * 4, ct, ctw * 4, ctw * 4, count, hipMemcpyDeviceToDevice, s);
-  if (err != hipSuccess) return err;
+  // rotations by 1 .. n1-1 (one ModUp per input).  Up to 2^14 the input's copy
+  // into slot 0 rides on the rotations' ModDown launch; else it is a copy of its own.
+  hipError_t err = hipSuccess;
+  const bool copy_in_rotation = n1 > 1 && t.log_n <= 14;
+  if (!copy_in_rotation) {
+    err = hipMemcpy2DAsync(baby, n1 * ctw * 4, ct, ctw * 4, ctw * 4, count, hipMemcpyDeviceToDevice, s);
+    if (err != hipSuccess) return err;
+  }
   if (n1 > 1) {
     RotPlan plan{n1 - 1, n1 - 1, 1, 1, 0};
+    const Seq slot0{1, n1, 0};
     err = launch_rotate_seq(t, ct, contiguous(), count, count * (n1 - 1), plan, ksk, rws, baby,
-                            Seq{n1 - 1, n1, 1}, s);
+                            Seq{n1 - 1, n1, 1}, s, copy_in_rotation ? &slot0 : nullptr);
     if (err != hipSuccess) return err;
   }
   // inner sums: the full-polynomial MAC (one input), or the register-tiled
@@ -895,7 +917,7 @@ hipError_t launch_bsgs(const Tables& t, const uint32_t* pt, const uint32_t* ct, 
   // baby region, free after the MAC)
   RotPlan plan{1, n2 - 1, n1, n1, 0};
   err = launch_rotate_seq(t, inner, Seq{n2 - 1, n2, 1}, count * (n2 - 1), count * (n2 - 1), plan,
-                          ksk + static_cast<size_t>(n1 - 1) * key_words, rws, nullptr, contiguous(), s);
+                          ksk + static_cast<size_t>(n1 - 1) * key_words, rws, nullptr, contiguous(), s, nullptr);
   if (err != hipSuccess) return err;
   const uint32_t* acc = rot_layout(t, count * (n2 - 1), count * (n2 - 1), rws).acc;
   giant_ext_kernel<<<static_cast<uint32_t>(count * 2 * (L + 1) * n / 64), kThreads, 0, s>>>(
