@@ -106,7 +106,8 @@ int ckks_intt(const ckks_ctx* ctx, uint32_t* polys, uint32_t count, uint32_t lim
  * packing):  w_enc[j][i][l] = rint(w[j][i] * scale) mod q_l, rint rounding
  * half to even.
  *   w      device fp64 [d_out][d_in]; |w * scale| < 2^63 and finite.
- *   w_enc  device uint32 [d_out][d_in][limbs]. */
+ *   w_enc  device uint32 [d_out][d_in][limbs]; must not overlap w
+ *          (CKKS_E_INVALID_ARG). */
 int ckks_linear_encode_scalar(const ckks_ctx* ctx, const double* w, uint32_t d_out,
                               uint32_t d_in, uint32_t limbs, double scale,
                               uint32_t* w_enc, void* stream);
@@ -116,7 +117,7 @@ int ckks_linear_encode_scalar(const ckks_ctx* ctx, const double* w, uint32_t d_o
  * exp(i pi 5^j / N), m_k = (2/N) Re sum_j z_j exp(-i pi 5^j k / N), then
  * p_k = rint(scale * m_k), reduced mod each q_l and taken to NTT form.
  *   slots  device fp64 [count][N/2] (real slot values).
- *   pt     device uint32 [count][limbs][N], NTT form.
+ *   pt     device uint32 [count][limbs][N], NTT form; must not overlap slots.
  * Supported for log_n <= 15 (CKKS_E_UNSUPPORTED above).  The spectral
  * transform runs in fp64, so a coefficient whose scaled value lies within
  * about 1e-9 of a rounding tie may differ by one from an exact evaluation. */
@@ -129,10 +130,15 @@ int ckks_linear_encode_poly(const ckks_ctx* ctx, const double* slots, uint32_t c
  *     ct_out[j][c][l][k] = sum_i w_enc[j][i][l] * ct_in[i][c][l][k]  mod q_l.
  *   w_enc    device uint32 [d_out][d_in][limbs], residues < q_l.
  *   ct_in    device uint32 [d_in][2][limbs][N].
- *   ct_out   device uint32 [d_out][2][limbs][N]; must not overlap ct_in/w_enc.
+ *   ct_out   device uint32 [d_out][2][limbs][N]; must not overlap ct_in or
+ *            w_enc (checked: CKKS_E_INVALID_ARG).
  *   workspace / workspace_bytes: device scratch of at least
  *            ckks_workspace_bytes(ctx, CKKS_OP_MAC_SCALAR, d_out, d_in, limbs)
- *            bytes (may be 0 for the VALU kernel); else CKKS_E_WORKSPACE.
+ *            bytes (may be 0 for the VALU kernel); else CKKS_E_WORKSPACE.  It
+ *            must not overlap ct_in, ct_out or w_enc (CKKS_E_INVALID_ARG).
+ * d_out <= 524280 and d_in <= 2^24 (else CKKS_E_INVALID_ARG); the matrix-core
+ * kernel takes d_in <= 4096 (above it CKKS_MAC_AUTO runs the VALU kernel and
+ * CKKS_MAC_MFMA returns CKKS_E_UNSUPPORTED).
  * d_out == 0 is a no-op; d_in == 0 writes zeros. */
 int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc,
                            const uint32_t* ct_in, uint32_t* ct_out, uint32_t d_out,
@@ -144,7 +150,8 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc,
  *     ct_out[j][c][l][k] = sum_i pt[j][i][l][k] * ct_in[i][c][l][k]  mod q_l,
  * i.e. a negacyclic product per pair in the coefficient domain.
  *   pt      device uint32 [d_out][d_in][limbs][N] (NTT form).
- *   ct_in   device uint32 [d_in][2][limbs][N];  ct_out [d_out][2][limbs][N]. */
+ *   ct_in   device uint32 [d_in][2][limbs][N];  ct_out [d_out][2][limbs][N],
+ *           which must not overlap pt or ct_in (CKKS_E_INVALID_ARG). */
 int ckks_linear_mac_poly(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* ct_in,
                          uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
                          void* stream);
@@ -154,9 +161,10 @@ int ckks_linear_mac_poly(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t
  * q_0..q_(limbs-1):  out = NTT_l( round(C / q_(limbs-1)) mod q_l ), l < limbs-1,
  * computed as (c_l - NTT_l([INTT(c_(limbs-1))]_centred mod q_l)) * q_(limbs-1)^-1.
  *   ct_in   device uint32 [count][2][limbs][N], limbs >= 2.
- *   ct_out  device uint32 [count][2][limbs-1][N]; must not overlap ct_in.
+ *   ct_out  device uint32 [count][2][limbs-1][N]; must not overlap ct_in
+ *           (checked: CKKS_E_INVALID_ARG).
  *   workspace: ckks_workspace_bytes(ctx, CKKS_OP_RESCALE, count, 0, limbs)
- *           bytes (0 for log_n <= 15). */
+ *           bytes (0 for log_n <= 15), not overlapping ct_in or ct_out. */
 int ckks_rescale(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t* ct_out,
                  uint32_t count, uint32_t limbs, void* workspace, size_t workspace_bytes,
                  void* stream);
@@ -248,9 +256,14 @@ int ckks_rotate(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t count, uint
  * d-periodically in the slots of each of `count` input ciphertexts ct_in
  * [count][2][Lk][N] (Halevi-Shoup diagonals with the baby-step / giant-step
  * split):  y = sum_j rot( sum_i pt[j][i] (.) rot(x, i), j n1 ), then one rescale.
- * The giant-step rotations are summed before their division by P: the sum is
- * formed over the L primes (P times the unrotated term and the rotated c0
- * parts, plus the key-switching inner products) and divided by P once.
+ * Schedule: the giant-step rotations are summed before their division by P
+ * (the sum is formed over the L primes: P times the unrotated term and the
+ * rotated c0 parts, plus the key-switching inner products, then divided by P
+ * once).  Against the formula with every rotation complete (its own division
+ * by P) this changes only roundings: the two results decrypt to values at
+ * most N + 1 apart per coefficient, and they are bit-identical unless a
+ * coefficient of the sum lies within n2/2 of a rounding boundary of the
+ * closing rescale.
  * pt [n2][n1][Lk][N]: NTT-form encodings of rot(diag_(j n1 + i), -j n1) (the
  * slot vectors diag_k[t] = W[t mod d][(t + k) mod d]; ckks_linear_encode_poly
  * makes them).  ksk: n1 - 1 rotation keys for steps 1 .. n1-1 followed by

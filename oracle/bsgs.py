@@ -18,15 +18,23 @@ giant-step split:
   The plaintexts pt[j, i] = Encode(rot(diag_{j n1 + i}, -j n1)) are the pre-encoded
   objects; one call takes n1 - 1 baby-step rotations of the input, n2 ct x pt inner
   sums (the full-polynomial MAC), n2 - 1 giant-step rotations, a sum, and one rescale.
-* The giant-step rotations are summed before their division by P (a lazy ModDown, as
-  BSGS implementations commonly do): with y_j the inner sums and (a0_j, a1_j) the
-  key-switching inner product of sigma_j(c1 of y_j) over q_0 .. q_{L-1}, P,
+* ``matvec`` is that formula as written: every rotation, baby or giant, is a complete
+  rotation (automorphism, then key switching with its own division by P, exactly
+  ``keyswitch.rotate``), the rotated inner sums are added mod Q, and the sum is
+  rescaled once.  It is the reference.
+* ``matvec_lazy`` is a schedule of the same product that an accelerator may prefer:
+  the giant-step rotations are summed before their division by P.  With y_j the inner
+  sums and (a0_j, a1_j) the key-switching inner product of sigma_j(c1 of y_j) over
+  q_0 .. q_{L-1}, P,
 
-      z = ModDown( P y_0 + sum_{j >= 1} ( (P sigma_j(c0 of y_j), 0) + (a0_j, a1_j) ) ),
+      z = ModDown( P y_0 + sum_{j >= 1} ( (P sigma_j(c0 of y_j), 0) + (a0_j, a1_j) ) ).
 
-  which equals the sum of the n2 rotated inner sums up to the rounding of one
-  division by P instead of n2 - 1 of them (P y is exact in the extended basis:
-  ModDown(P y + a) = y + ModDown(a)).  Then z is rescaled once.
+  P y is exact in the extended basis (ModDown(P y + a) = y + ModDown(a)), so z differs
+  from the eager sum only in rounding: one division by P of the summed inner products
+  instead of one per giant step, at most n2 / 2 per coefficient of each component.
+  After the closing rescale the two results decrypt to values at most N + 1 apart per
+  coefficient (both rescale roundings included); ``eager_lazy_bound`` states it and the
+  tests pin it.  The lazy form is an implementation choice, not a reading of the paper.
 
 Tiling (section 3.3's small-ring tiles, section 6's GEMM tiling experiment): a
 D x K weight matrix cut into a t_o x t_i grid of d x d tiles (d = D / t_o = K / t_i)
@@ -36,7 +44,9 @@ q_l per limb), each tile product a BSGS product as above.
 
 Parity: pinned (tests/test_oracle_keyswitch.py) by decrypting and decoding the result
 against numpy's W @ x, by the plaintext identity of the diagonal split on random
-matrices, and (tiles) by decoding the aggregated blocks against W @ x.
+matrices, by the eager product's agreement with an independent composition of single
+rotations (``keyswitch.rotate``) and plaintext products, and (tiles) by decoding the
+aggregated blocks against W @ x.
 """
 from __future__ import annotations
 
@@ -69,21 +79,64 @@ def replicate(x, slots: int) -> np.ndarray:
     return x[np.arange(slots) % len(x)]
 
 
-def matvec(pt, ct, n1: int, keys, qs_p, psis_p, log_n: int) -> np.ndarray:
-    """BSGS product of the encoded diagonals pt (n2, n1, L, N) with ct (2, L, N).
+def _baby_and_inner(pt, ct, n1: int, keys, qs_p, psis_p, log_n: int):
+    """The baby-step rotations rot(x, i), i < n1, and the n2 inner sums
+    y_j = sum_i pt[j, i] (.) rot(x, i) (2, L, N) each."""
+    L = ct.shape[1]
+    baby = [np.asarray(ct, dtype=np.uint64)]
+    for i in range(1, n1):
+        baby.append(rotate(baby[0], i, keys[i], qs_p, psis_p, log_n))
+    return mac_poly(pt, np.stack(baby), qs_p[:L])          # (n2, 2, L, N)
+
+
+def matvec(pt, ct, n1: int, keys, qs_p, psis_p, log_n: int, rescaled: bool = True) -> np.ndarray:
+    """BSGS product of the encoded diagonals pt (n2, n1, L, N) with ct (2, L, N), every
+    rotation complete (its own key switch and division by P), then one rescale.
 
     keys: rotation keys by step r (rotation_key(s, r)) for r = 1 .. n1-1 and
     r = j n1, j = 1 .. n2-1; qs_p / psis_p: the L ciphertext primes and the special
-    prime last.  Returns the rescaled result (2, L-1, N).
+    prime last.  Returns the rescaled result (2, L-1, N), or with rescaled=False the
+    sum before the closing rescale (2, L, N).
     """
     pt = np.asarray(pt)
     n2 = pt.shape[0]
     L = ct.shape[1]
     qs = qs_p[:L]
-    baby = [np.asarray(ct, dtype=np.uint64)]
-    for i in range(1, n1):
-        baby.append(rotate(baby[0], i, keys[i], qs_p, psis_p, log_n))
-    inner = mac_poly(pt, np.stack(baby), qs)              # (n2, 2, L, N)
+    inner = _baby_and_inner(pt, ct, n1, keys, qs_p, psis_p, log_n)
+    q = np.array(qs, dtype=np.uint64)[:, None]
+    z = inner[0] % q
+    for j in range(1, n2):
+        z = (z + rotate(inner[j], j * n1, keys[j * n1], qs_p, psis_p, log_n)) % q
+    return rescale(z[None], qs, psis_p[:L], log_n)[0] if rescaled else z
+
+
+def eager_lazy_bound(n2: int, log_n: int, q_last: int) -> int:
+    """Largest difference, per coefficient, between the decryptions (under the ternary
+    key s) of ``matvec`` and ``matvec_lazy`` on the same inputs.
+
+    Before the closing rescale the two sums differ by delta with |delta_c| <= n2 / 2 per
+    coefficient of each component c (n2 - 1 roundings of a division by P against one),
+    so their decryptions differ by at most (n2 / 2)(1 + N).  Rescaling z to (z - r) / q
+    with centred remainders |r_c| <= (q - 1) / 2 gives decryptions
+    (dec(z) - r_0 - r_1 s) / q, so the results differ by at most
+    ((n2 / 2) (1 + N) + (q - 1)(1 + N)) / q < (N + 1)(1 + n2 / (2 q)), i.e. N + 1 when
+    n2 < q / (N + 1).  (The rescaled results are in fact bit-identical unless a
+    coefficient of the sum lies within n2 / 2 of a rounding boundary of the closing
+    rescale, which happens with probability about 2 N n2 / q per product.)"""
+    n = 1 << log_n
+    num = (n2 * (1 + n) + 1) // 2 + (q_last - 1) * (1 + n)
+    return num // q_last                                    # the difference is an integer
+
+
+def matvec_lazy(pt, ct, n1: int, keys, qs_p, psis_p, log_n: int, rescaled: bool = True) -> np.ndarray:
+    """The same product with the giant-step rotations summed before one division by P
+    (see the module text); equal to ``matvec`` within ``eager_lazy_bound`` after
+    decryption.  rescaled=False: the sum before the closing rescale."""
+    pt = np.asarray(pt)
+    n2 = pt.shape[0]
+    L = ct.shape[1]
+    qs = qs_p[:L]
+    inner = _baby_and_inner(pt, ct, n1, keys, qs_p, psis_p, log_n)
     P = qs_p[-1]
     qp = np.array(qs_p, dtype=np.uint64)[:, None]
     ext = np.zeros((2, L + 1, 1 << log_n), dtype=np.uint64)    # over q_0 .. q_{L-1}, P
@@ -100,7 +153,7 @@ def matvec(pt, ct, n1: int, keys, qs_p, psis_p, log_n: int) -> np.ndarray:
         add_times_p(0, sig[0])
         ext = (ext + keyswitch_ext(sig[1], keys[j * n1], qs_p, psis_p, log_n)) % qp
     z = rescale(ext[None], qs_p, psis_p, log_n)[0]              # one division by P
-    return rescale(z[None], qs, psis_p[:L], log_n)[0]
+    return rescale(z[None], qs, psis_p[:L], log_n)[0] if rescaled else z
 
 
 def tile_slots(W, t_o: int, t_i: int, n1: int, slots: int) -> np.ndarray:
@@ -113,9 +166,11 @@ def tile_slots(W, t_o: int, t_i: int, n1: int, slots: int) -> np.ndarray:
                                for j in range(t_i)]) for i in range(t_o)])
 
 
-def tiled_matvec(pt, cts, n1: int, keys, qs_p, psis_p, log_n: int) -> np.ndarray:
+def tiled_matvec(pt, cts, n1: int, keys, qs_p, psis_p, log_n: int, product=None) -> np.ndarray:
     """Tile products summed per output block: pt (t_o, t_i, n2, n1, L, N), cts (t_i, 2, L, N)
-    (the encrypted input blocks).  Returns (t_o, 2, L-1, N)."""
+    (the encrypted input blocks).  product: the per-tile BSGS product (``matvec`` by
+    default).  Returns (t_o, 2, L-1, N)."""
+    product = matvec if product is None else product
     pt = np.asarray(pt)
     t_o, t_i = pt.shape[:2]
     L = cts.shape[2]
@@ -124,7 +179,7 @@ def tiled_matvec(pt, cts, n1: int, keys, qs_p, psis_p, log_n: int) -> np.ndarray
     for i in range(t_o):
         acc = None
         for j in range(t_i):
-            y = matvec(pt[i, j], cts[j], n1, keys, qs_p, psis_p, log_n)
+            y = product(pt[i, j], cts[j], n1, keys, qs_p, psis_p, log_n)
             acc = y if acc is None else (acc + y) % q
         out.append(acc)
     return np.stack(out)

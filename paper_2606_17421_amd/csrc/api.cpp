@@ -171,6 +171,12 @@ struct Blob {
   }
 };
 
+// Byte ranges [x, x + xb) and [y, y + yb) share at least one byte.
+bool overlaps(const void* x, size_t xb, const void* y, size_t yb) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(x), b0 = reinterpret_cast<uintptr_t>(y);
+  return xb != 0 && yb != 0 && a0 < b0 + yb && b0 < a0 + xb;
+}
+
 int check_ctx(const ckks_ctx* ctx) {
   if (!ctx) return fail(CKKS_E_INVALID_ARG, "null context");
   return CKKS_OK;
@@ -439,6 +445,7 @@ int ckks_linear_encode_scalar(const ckks_ctx* ctx, const double* w, uint32_t d_o
   if (count == 0) return ok();
   if (int rc = check_ptr(w, "w")) return rc;
   if (int rc = check_ptr(w_enc, "w_enc")) return rc;
+  if (overlaps(w_enc, count * limbs * 4, w, count * 8)) return fail(CKKS_E_INVALID_ARG, "w_enc overlaps w");
   DeviceGuard guard(ctx->device);
   hipError_t e = ckks::launch_encode_scalar(ctx->t, w, count, limbs, scale, w_enc,
                                             static_cast<hipStream_t>(stream));
@@ -454,16 +461,20 @@ int ckks_linear_encode_poly(const ckks_ctx* ctx, const double* slots, uint32_t c
   if (count == 0) return ok();
   if (int rc = check_ptr(slots, "slots")) return rc;
   if (int rc = check_ptr(pt, "pt")) return rc;
+  if (overlaps(pt, size_t(count) * limbs * ctx->n * 4, slots, size_t(count) * (ctx->n / 2) * 8))
+    return fail(CKKS_E_INVALID_ARG, "pt overlaps slots");
   DeviceGuard guard(ctx->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = ckks::launch_encode_poly(ctx->t, slots, count, limbs, scale, pt, s);
   return e == hipSuccess ? ok() : hip_fail(e, "encode_poly launch");
 }
 
-static int check_mac_shapes(const ckks_ctx* ctx, uint32_t d_out, uint32_t d_in) {
-  if (d_out > (65535u * 8u)) return fail(CKKS_E_INVALID_ARG, "d_out=%u too large", d_out);
-  (void)ctx;
-  (void)d_in;
+// Shape limits of the scalar MAC: the VALU kernel's grid has ceil(d_out / 8)
+// rows (at most 65535), and d_in is bounded so that every weight and fragment
+// offset of both kernels stays far inside its index type.
+static int check_mac_shapes(uint32_t d_out, uint32_t d_in) {
+  if (d_out > (65535u * 8u)) return fail(CKKS_E_INVALID_ARG, "d_out=%u too large (max %u)", d_out, 65535u * 8u);
+  if (d_in > ckks::kMaxMacDin) return fail(CKKS_E_INVALID_ARG, "d_in=%u too large (max %u)", d_in, ckks::kMaxMacDin);
   return CKKS_OK;
 }
 
@@ -472,12 +483,17 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc, const uin
                            void* workspace, size_t workspace_bytes, void* stream) {
   if (int rc = check_ctx(ctx)) return rc;
   if (int rc = check_limbs(ctx, limbs, 1)) return rc;
-  if (int rc = check_mac_shapes(ctx, d_out, d_in)) return rc;
+  if (int rc = check_mac_shapes(d_out, d_in)) return rc;
   if (d_out == 0) return ok();
   if (int rc = check_ptr(ct_out, "ct_out")) return rc;
+  const size_t ct_row = size_t(2) * limbs * ctx->n * 4;  // bytes of one ciphertext
+  const size_t out_b = size_t(d_out) * ct_row, in_b = size_t(d_in) * ct_row;
+  const size_t w_b = size_t(d_out) * d_in * limbs * 4;
   if (d_in > 0) {
     if (int rc = check_ptr(w_enc, "w_enc")) return rc;
     if (int rc = check_ptr(ct_in, "ct_in")) return rc;
+    if (overlaps(ct_out, out_b, ct_in, in_b) || overlaps(ct_out, out_b, w_enc, w_b))
+      return fail(CKKS_E_INVALID_ARG, "ct_out overlaps ct_in or w_enc");
   }
   DeviceGuard guard(ctx->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -495,6 +511,9 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc, const uin
     if (!workspace || workspace_bytes < need)
       return fail(CKKS_E_WORKSPACE, "MAC workspace %zu bytes < %zu required", workspace_bytes, need);
     if (!aligned16(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 16-byte aligned");
+    if (overlaps(workspace, need, ct_out, out_b) || overlaps(workspace, need, ct_in, in_b) ||
+        overlaps(workspace, need, w_enc, w_b))
+      return fail(CKKS_E_INVALID_ARG, "workspace overlaps ct_in, ct_out or w_enc");
     e = ckks::launch_mac_scalar_mfma(ctx->t, w_enc, ct_in, ct_out, d_out, d_in, limbs, workspace, s);
   } else {
     e = ckks::launch_mac_scalar_valu(ctx->t, w_enc, ct_in, ct_out, d_out, d_in, limbs, s);
@@ -514,6 +533,10 @@ int ckks_linear_mac_poly(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t
   if (d_in > 0) {
     if (int rc = check_ptr(pt, "pt")) return rc;
     if (int rc = check_ptr(ct_in, "ct_in")) return rc;
+    const size_t ct_row = size_t(2) * limbs * ctx->n * 4, out_b = size_t(d_out) * ct_row;
+    if (overlaps(ct_out, out_b, ct_in, size_t(d_in) * ct_row) ||
+        overlaps(ct_out, out_b, pt, size_t(d_out) * d_in * limbs * ctx->n * 4))
+      return fail(CKKS_E_INVALID_ARG, "ct_out overlaps ct_in or pt");
   }
   DeviceGuard guard(ctx->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -534,6 +557,10 @@ int ckks_rescale(const ckks_ctx* ctx, const uint32_t* ct_in, uint32_t* ct_out, u
   if (need && (!workspace || workspace_bytes < need))
     return fail(CKKS_E_WORKSPACE, "rescale workspace %zu bytes < %zu required", workspace_bytes, need);
   if (need && !aligned16(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 16-byte aligned");
+  const size_t in_b = size_t(count) * 2 * limbs * ctx->n * 4, out_b = size_t(count) * 2 * (limbs - 1) * ctx->n * 4;
+  if (overlaps(ct_out, out_b, ct_in, in_b)) return fail(CKKS_E_INVALID_ARG, "ct_out overlaps ct_in");
+  if (need && (overlaps(workspace, need, ct_in, in_b) || overlaps(workspace, need, ct_out, out_b)))
+    return fail(CKKS_E_INVALID_ARG, "workspace overlaps ct_in or ct_out");
   DeviceGuard guard(ctx->device);
   hipError_t e = ckks::launch_rescale(ctx->t, ct_in, ct_out, count, limbs, workspace,
                                       static_cast<hipStream_t>(stream));
@@ -547,11 +574,6 @@ static int check_rows(const ckks_ctx* ctx, uint32_t count, uint32_t limbs) {
   if (rows > 0x7FFFFFFFull / (ctx->log_n == 16 ? 64 : 1))
     return fail(CKKS_E_INVALID_ARG, "too many polynomials (%zu rows)", rows);
   return CKKS_OK;
-}
-
-static bool overlaps(const void* x, size_t xb, const void* y, size_t yb) {
-  const uintptr_t a0 = reinterpret_cast<uintptr_t>(x), b0 = reinterpret_cast<uintptr_t>(y);
-  return a0 < b0 + yb && b0 < a0 + xb;
 }
 
 int ckks_encrypt(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* s_ntt, const uint32_t* a,

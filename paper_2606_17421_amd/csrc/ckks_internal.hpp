@@ -12,6 +12,7 @@ namespace ckks {
 constexpr int kMaxLimbs = 16;
 constexpr int kMinLogN = 10;
 constexpr int kMaxLogN = 16;
+constexpr uint32_t kMaxMacDin = 1u << 24;  // largest d_in of the scalar MAC entry point
 
 // Per-context device tables.  All arrays live in one device allocation owned
 // by the context; [L][N] arrays are limb-major.

@@ -98,21 +98,46 @@ def plan(groups, budget_bytes: int, full_limbs: int, n: int, min_out_limbs: int 
     return p
 
 
+def _span(t):
+    """Byte range [start, end) of a tensor's storage view."""
+    start = t.data_ptr()
+    return start, start + t.numel() * t.element_size()
+
+
+def check_refresh_draws(draws, needed: int) -> None:
+    """The randomness of a pass's refreshes: at least `needed` (a, e) pairs, and no
+    two pairs sharing storage.  A refresh is Enc(Dec(ct)) (section 3.2); encrypting
+    two different plaintexts with the same (a, e) would hand the untrusted side the
+    difference of the plaintexts (c0 - c0' = m - m'), so every refresh takes its own."""
+    draws = list(draws)
+    if len(draws) < needed:
+        raise ValueError(f"the plan has {needed} refreshes but {len(draws)} (a, e) draws were given")
+    spans = []
+    for k, (a, e) in enumerate(draws[:needed]):
+        for t in (a, e):
+            lo, hi = _span(t)
+            for lo2, hi2, k2 in spans:
+                if lo < hi2 and lo2 < hi:
+                    raise ValueError(f"refresh draws {k2} and {k} share storage: each refresh needs fresh (a, e)")
+            spans.append((lo, hi, k))
+
+
 class Executor:
     """Runs a Plan on the GPU through the library's entry points.
 
     weights: per group a cuda float64 tensor [d_out * d_in][N/2] of slot values
     (kept for fallback groups; pinned groups are encoded once here).
-    secret: dict with s_ntt (cuda [full_limbs][N]), and fresh randomness for
-    each refresh: a (cuda [max_d][full_limbs][N]) and e (cuda int32 [max_d][N]).
+    s_ntt: the secret in NTT form, cuda [full_limbs][N] (the refreshes run on the
+    trusted side of each boundary crossing).  The randomness of the refreshes is
+    an argument of run(), drawn anew by the caller for every pass.
     """
 
-    def __init__(self, ctx, the_plan: Plan, weights, scale: float, secret, stream=None):
+    def __init__(self, ctx, the_plan: Plan, weights, scale: float, s_ntt, stream=None):
         import torch
 
         import paper_2606_17421_amd as ck
         self.ck, self.ctx, self.plan, self.scale, self.stream = ck, ctx, the_plan, scale, stream
-        self.secret = secret
+        self.s_ntt = s_ntt
         n = ctx.n
         self.full_limbs = max(s.level for s in the_plan.steps)
         self.pts, self.slots = [], []
@@ -133,12 +158,18 @@ class Executor:
         d_max = max(max(s.group.d_out, s.group.d_in) for s in the_plan.steps)
         self.buf = [ck.empty_u32((d_max * 2 * self.full_limbs * n,), device=ctx.device) for _ in range(3)]
 
-    def run(self, ct_in, events=None):
-        """One pass over the plan.  ct_in: cuda [d_in][2][full_limbs][N].  Returns the
-        output tensor (a view into an internal buffer, [d_out][2][limbs][N]) and its limbs.
+    def run(self, ct_in, refresh_draws=(), events=None):
+        """One pass over the plan.  ct_in: cuda [d_in][2][full_limbs][N].
+        refresh_draws: one (a, e) pair per refresh of the plan, in plan order, each
+        freshly drawn for this pass (a: cuda [d_out][full_limbs][N] uniform residues in
+        NTT form; e: cuda int32 [d_out][N] error coefficients); pairs must not share
+        storage.  Returns the output tensor (a view into an internal buffer,
+        [d_out][2][limbs][N]) and its limbs.
         events: optional list; per step a (start, after_encode, end) triple of cuda events."""
         import torch
         ck, ctx, n, st = self.ck, self.ctx, self.ctx.n, self.stream
+        check_refresh_draws(refresh_draws, self.plan.refreshes)
+        draws = iter(refresh_draws)
         cur, limbs = ct_in, self.plan.steps[0].level
         # buffers: 0 = MAC output, 1 = rescale output, 2 = refresh output; a group's
         # input (1 or 2, or ct_in) is consumed by its MAC before 1 is rewritten
@@ -161,8 +192,8 @@ class Executor:
             cur, limbs = res, limbs - 1
             if s.refresh_after:
                 out = self.buf[2][: g.d_out * 2 * self.full_limbs * n]
-                sec = self.secret
-                ck.ckks_refresh(ctx, res, limbs, sec["s_ntt"], sec["a"], sec["e"], g.d_out, self.full_limbs, out, st)
+                a, e = next(draws)
+                ck.ckks_refresh(ctx, res, limbs, self.s_ntt, a, e, g.d_out, self.full_limbs, out, st)
                 cur, limbs = out, self.full_limbs
             if ev is not None:
                 ev[2].record(st if st is not None else torch.cuda.current_stream())

@@ -142,3 +142,60 @@ def test_mac_poly_ragged_row_group(gpu_lib):
     out = ck.empty_u32((d_out, 2, limbs, n))
     ck.ckks_linear_mac_poly(ctx, ck.to_device(pt), ck.to_device(ct), out, d_out, d_in, limbs)
     assert np.array_equal(ck.to_host_u32(out), OL.mac_poly(pt, ct, qs).astype(np.uint32))
+
+
+def _expect_invalid(ck, fn, *args, **kw):
+    with pytest.raises(ck.CkksError) as e:
+        fn(*args, **kw)
+    assert e.value.code == ck.CKKS_E_INVALID_ARG, e.value
+
+
+def test_overlapping_outputs_are_rejected(gpu_lib):
+    """Outputs that share bytes with an input (in place, or offset by one
+    ciphertext) and workspaces that share bytes with a data buffer are refused on
+    the host with CKKS_E_INVALID_ARG, before any launch."""
+    import torch
+    ck = gpu_lib
+    log_n, L, d = 10, 3, 4
+    ctx = ctx_for(ck, log_n, L)
+    n = ctx.n
+    ct_words = 2 * L * n
+    big = ck.empty_u32((4 * d * ct_words,))
+    w = ck.empty_u32((d, d, L))
+    ws_bytes = ck.ckks_workspace_bytes(ctx, ck.CKKS_OP_MAC_SCALAR, d, d, L)
+    ws = ck.empty_u32((ws_bytes // 4 + 4,))
+    ct_in = big[: d * ct_words]
+    mac = ck.ckks_linear_mac_scalar
+    _expect_invalid(ck, mac, ctx, w, ct_in, ct_in, d, d, L, ws)                                  # in place
+    _expect_invalid(ck, mac, ctx, w, ct_in, big[ct_words: (d + 1) * ct_words], d, d, L, ws)      # partial
+    w_words = ck.empty_u32((d * ct_words,))
+    _expect_invalid(ck, mac, ctx, w_words[: d * d * L], ck.empty_u32((d * ct_words,)), w_words, d, d, L, ws)
+    out = big[d * ct_words: 2 * d * ct_words]
+    _expect_invalid(ck, mac, ctx, w, ct_in, out, d, d, L, big[2 * d * ct_words - 8:])           # ws over ct_out
+    _expect_invalid(ck, mac, ctx, w, ct_in, out, d, d, L, big[: ws_bytes // 4 + 4])            # ws over ct_in
+    pt = ck.empty_u32((d, d, L, n))
+    _expect_invalid(ck, ck.ckks_linear_mac_poly, ctx, pt, ct_in, ct_in, d, d, L)
+    _expect_invalid(ck, ck.ckks_linear_mac_poly, ctx, pt, ct_in, big[ct_words: (d + 1) * ct_words], d, d, L)
+    _expect_invalid(ck, ck.ckks_linear_mac_poly, ctx, pt, ct_in, pt.view(-1)[: d * ct_words], d, d, L)
+    _expect_invalid(ck, ck.ckks_rescale, ctx, ct_in, ct_in, d, L)
+    _expect_invalid(ck, ck.ckks_rescale, ctx, ct_in, big[ct_words // 2: ct_words // 2 + d * 2 * (L - 1) * n], d, L)
+    wf = ck.empty_u32((2 * d * d * L,))
+    _expect_invalid(ck, ck.ckks_linear_encode_scalar, ctx, wf.view(torch.float64), d, d, L, 2.0 ** 20, wf[: d * d * L])
+    slots = torch.empty((2, n // 2), dtype=torch.float64, device="cuda")
+    _expect_invalid(ck, ck.ckks_linear_encode_poly, ctx, slots, 2, 1, 2.0 ** 20, slots.view(torch.int32))
+    # disjoint buffers still work
+    mac(ctx, w, ct_in, out, d, d, L, ws)
+
+
+def test_mac_rejects_oversized_d_in(gpu_lib):
+    """d_in above 2^24 is refused on the host (CKKS_E_INVALID_ARG); the shape check
+    runs before any buffer is looked at, so tiny buffers suffice."""
+    import ctypes
+    ck = gpu_lib
+    ctx = ctx_for(ck, 10, 2)
+    buf = ck.empty_u32((64,))
+    rc = ck._lib.ckks_linear_mac_scalar(ctx.handle, ctypes.c_void_p(buf.data_ptr()), ctypes.c_void_p(buf.data_ptr()),
+                                        ctypes.c_void_p(buf.data_ptr() + 128), 1, (1 << 24) + 1, 2, None, 0,
+                                        ctypes.c_void_p(0))
+    assert rc == ck.CKKS_E_INVALID_ARG
+    assert "d_in" in ck.ckks_last_error()

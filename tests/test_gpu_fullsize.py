@@ -83,12 +83,11 @@ def test_scalar_layer_full_size(gpu_lib, key):
     say(f"[{key}] oracle MAC done {time.time() - t0:.1f}s")
     for r, j in enumerate(rows):
         assert np.array_equal(mac_rows[r], refs[r].astype(np.uint32)), f"MAC row {j}"
-    sub = rows if cfg.log_n <= 14 else [rows[0], rows[5], rows[10], rows[-1]]
     with ThreadPoolExecutor(POOL) as ex:
-        rres = list(ex.map(lambda j: OL.rescale(refs[rows.index(j)][None], qs, psis, cfg.log_n)[0], sub))
-    say(f"[{key}] oracle rescale done {time.time() - t0:.1f}s")
-    for j, want in zip(sub, rres):
-        assert np.array_equal(res_rows[rows.index(j)], want.astype(np.uint32)), f"rescale row {j}"
+        rres = list(ex.map(lambda r: OL.rescale(refs[r][None], qs, psis, cfg.log_n)[0], range(len(rows))))
+    say(f"[{key}] oracle rescale of all {len(rows)} sampled rows done {time.time() - t0:.1f}s")
+    for r, j in enumerate(rows):
+        assert np.array_equal(res_rows[r], rres[r].astype(np.uint32)), f"rescale row {j}"
 
     if key == "c3":
         # standalone batched transforms over all 3072*2*6 output polynomials
@@ -157,15 +156,66 @@ def test_fallback_layer_full_size(gpu_lib):
     for j in range(d):
         assert np.array_equal(mac_h[j], refs[j].astype(np.uint32)), f"MAC row {j}"
     say(f"[c5] oracle MAC done {time.time() - t0:.1f}s")
-    sub = [0, 17, 40, d - 1]
     with ThreadPoolExecutor(POOL) as ex:
-        rres = list(ex.map(lambda j: OL.rescale(refs[j][None], layer.qs, layer.psis, cfg.log_n)[0], sub))
-    for j, want in zip(sub, rres):
-        assert np.array_equal(res_h[j], want.astype(np.uint32)), f"rescale row {j}"
+        rres = list(ex.map(lambda j: OL.rescale(refs[j][None], layer.qs, layer.psis, cfg.log_n)[0], range(d)))
+    for j in range(d):
+        assert np.array_equal(res_h[j], rres[j].astype(np.uint32)), f"rescale row {j}"
+    say(f"[c5] oracle rescale of all {d} outputs done {time.time() - t0:.1f}s")
+    sub = [0, 17, 40, d - 1]
     # decrypt sampled outputs: slot-wise sum_i W[j,i] * x_i within the rescale noise
     scale_out = cfg.scale * cfg.scale / layer.qs[-1]
     ref = np.stack([np.einsum("is,is->s", layer.W[j], layer.X) for j in sub])
     chk = check_decrypted(layer, res_h[sub], sub, ref, scale_out)
     say(f"[c5] decrypt check {chk} {time.time() - t0:.1f}s")
     assert chk["ok"], chk
+    ctx.close()
+
+
+def test_fallback_encode_every_weight_constant_slots(gpu_lib):
+    """Config 5's shape, every one of its 64 x 64 weights through the full-polynomial
+    encode on a call of its own: with constant slot vectors (slot value W[j, i]) the
+    encoding is the constant polynomial rint(W[j, i] scale), whose NTT is that constant
+    in every slot, i.e. exactly the scalar encoding.  So all 4096 plaintexts must equal
+    the oracle's scalar encodings broadcast over the N slots, and the poly MAC over them
+    must equal the scalar MAC bit for bit on all 64 outputs (and the oracle's scalar MAC
+    on sampled outputs)."""
+    import torch
+    ck = gpu_lib
+    cfg = get("c5")
+    t0 = time.time()
+    ctx = ck.Context(cfg.log_n, cfg.limbs)
+    qs = ctx.moduli
+    L, n, d = cfg.limbs, cfg.n, cfg.d_in
+    st = gen.streams(cfg.index, 77)
+    Wc = gen.scalar_weights(st["weights"], d, d)                        # (64, 64) N(0, 0.02^2)
+    ct = gen.uniform_residues(st["residues"], (d, 2), qs, n)
+    w_ref = OE.encode_scalar(Wc, cfg.scale, qs)                          # (64, 64, L) oracle
+    slots = ck.to_device(Wc.reshape(d * d, 1)).expand(d * d, n // 2).contiguous()
+    pt = ck.empty_u32((d, d, L, n))
+    ck.ckks_linear_encode_poly(ctx, slots, d * d, L, cfg.scale, pt)
+    del slots
+    want = ck.to_device(w_ref.astype(np.uint32)).view(d, d, L, 1)
+    bad = int((pt != want).sum())
+    say(f"[c5 constant slots] {d * d} weights x {L} limbs x {n} slots encoded; mismatches {bad} "
+        f"{time.time() - t0:.1f}s")
+    assert bad == 0
+    d_ct = ck.to_device(ct)
+    out_poly = ck.empty_u32((d, 2, L, n))
+    ck.ckks_linear_mac_poly(ctx, pt, d_ct, out_poly, d, d, L)
+    w_enc = ck.empty_u32((d, d, L))
+    ck.ckks_linear_encode_scalar(ctx, ck.to_device(Wc), d, d, L, cfg.scale, w_enc)
+    ws = ck.empty_u32((ck.ckks_workspace_bytes(ctx, ck.CKKS_OP_MAC_SCALAR, d, d, L) // 4 + 4,))
+    out_scalar = ck.empty_u32((d, 2, L, n))
+    ck.ckks_linear_mac_scalar(ctx, w_enc, d_ct, out_scalar, d, d, L, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(ck.to_host_u32(w_enc), w_ref.astype(np.uint32))
+    assert torch.equal(out_poly, out_scalar), "poly MAC over constant-slot plaintexts != scalar MAC"
+    rows = gen.sample_rows(st["sample"], d, count=4)
+    got = _rows_host(ck, out_poly, rows)
+    with ThreadPoolExecutor(POOL) as ex:
+        refs = list(ex.map(lambda j: OL.mac_scalar(w_ref, ct, qs, rows=[j])[0], rows))
+    for r, j in enumerate(rows):
+        assert np.array_equal(got[r], refs[r].astype(np.uint32)), f"MAC row {j}"
+    say(f"[c5 constant slots] poly MAC = scalar MAC on all {d} outputs, oracle rows {rows} "
+        f"{time.time() - t0:.1f}s")
     ctx.close()

@@ -19,23 +19,25 @@ def model(d, layers):
     return [LinearGroup(f"g{i}", d, d, tee_after=(i == 1)) for i in range(layers)]
 
 
-def secret_inputs(ck, ctx, d, seed):
+def secret_inputs(ck, ctx, d, seed, refreshes):
+    """Secret (host and NTT form on the device), one fresh (a, e) draw per refresh
+    (host arrays and device tensors) and the input ciphertexts."""
     qs, n = ctx.moduli, ctx.n
     st = gen.streams(seed, LOG_N)
     s = gen.ternary_secret(st["secret"], n)
     s_res = np.stack([np.mod(s, q) for q in qs]).astype(np.uint32)
     s_ntt = ck.to_device(s_res)
     ck.ckks_ntt(ctx, s_ntt, 1, L)
-    a = gen.uniform_residues(st["residues"], (d,), qs, n)
-    e = gen.gaussian_error(st["error"], (d, n)).astype(np.int32)
+    draws = [(gen.uniform_residues(st["residues"], (d,), qs, n), gen.gaussian_error(st["error"], (d, n)).astype(np.int32))
+             for _ in range(refreshes)]
     ct = gen.uniform_residues(st["residues"], (d, 2), qs, n)
-    return s, a, e, ct, {"s_ntt": s_ntt, "a": ck.to_device(a), "e": ck.to_device(e)}
+    return s, s_ntt, draws, [(ck.to_device(a), ck.to_device(e)) for a, e in draws], ct
 
 
-def run(ck, ctx, groups, budget, weights_dev, sec, ct_dev):
+def run(ck, ctx, groups, budget, weights_dev, s_ntt, draws_dev, ct_dev):
     p = plan(groups, budget, L, ctx.n)
-    ex = Executor(ctx, p, weights_dev, SCALE, sec)
-    out, limbs = ex.run(ct_dev)
+    ex = Executor(ctx, p, weights_dev, SCALE, s_ntt)
+    out, limbs = ex.run(ct_dev, draws_dev)
     d = groups[-1].d_out
     return p, ck.to_host_u32(out[: d * 2 * limbs * ctx.n]).reshape(d, 2, limbs, ctx.n)
 
@@ -48,17 +50,38 @@ def test_result_does_not_depend_on_the_budget(gpu_lib):
     st = gen.streams(501, LOG_N)
     W = [gen.poly_weights(st["weights"], d, d, ctx.n // 2).reshape(d * d, ctx.n // 2) for _ in range(layers)]
     Wd = [ck.to_device(np.ascontiguousarray(w)) for w in W]
-    s, a, e, ct, sec = secret_inputs(ck, ctx, d, 502)
-    ct_dev = ck.to_device(ct)
     full = plan(groups, 1 << 40, L, ctx.n)
+    s, s_ntt, draws, draws_dev, ct = secret_inputs(ck, ctx, d, 502, full.refreshes)
+    ct_dev = ck.to_device(ct)
     outs = {}
     for budget in (1 << 40, 0, full.steps[0].encoded_bytes + full.steps[1].encoded_bytes):
-        p, outs[budget] = run(ck, ctx, groups, budget, Wd, sec, ct_dev)
+        p, outs[budget] = run(ck, ctx, groups, budget, Wd, s_ntt, draws_dev, ct_dev)
         assert p.pinned + p.fallback == layers
     ref = outs[1 << 40]
     for budget, o in outs.items():
         assert np.array_equal(o, ref), budget
     assert plan(groups, 0, L, ctx.n).fallback == layers
+
+
+def test_executor_refuses_reused_refresh_randomness(gpu_lib):
+    """Every refresh of a pass takes its own (a, e): too few draws, or two draws that
+    share storage, are refused before anything runs."""
+    import pytest as _pt
+    ck = gpu_lib
+    ctx = ck.Context(LOG_N, L)
+    d, layers = 4, 5
+    groups = model(d, layers)
+    p = plan(groups, 1 << 40, L, ctx.n)
+    assert p.refreshes >= 2
+    rng = np.random.default_rng(507)
+    W = [ck.to_device(gen.poly_weights(rng, d, d, ctx.n // 2).reshape(d * d, ctx.n // 2)) for _ in range(layers)]
+    s, s_ntt, draws, draws_dev, ct = secret_inputs(ck, ctx, d, 508, p.refreshes)
+    ex = Executor(ctx, p, W, SCALE, s_ntt)
+    with _pt.raises(ValueError):
+        ex.run(ck.to_device(ct), draws_dev[:-1])
+    with _pt.raises(ValueError):
+        ex.run(ck.to_device(ct), [draws_dev[0]] * p.refreshes)
+    ex.run(ck.to_device(ct), draws_dev)
 
 
 def test_chain_equals_the_oracle_composition(gpu_lib):
@@ -67,20 +90,24 @@ def test_chain_equals_the_oracle_composition(gpu_lib):
     ck = gpu_lib
     ctx = ck.Context(LOG_N, L)
     qs, psis, n = ctx.moduli, ctx.roots, ctx.n
-    d, layers = 4, 4
+    d, layers = 4, 5                       # two refreshes: after the TEE window and when the level runs out
     groups = model(d, layers)
     rng = np.random.default_rng(503)
     consts = [rng.normal(0, 0.02, (d, d)) for _ in range(layers)]
     W = [np.repeat(c.reshape(d * d, 1), n // 2, axis=1) for c in consts]
-    s, a, e, ct, sec = secret_inputs(ck, ctx, d, 504)
-    p, got = run(ck, ctx, groups, 1 << 40, [ck.to_device(w) for w in W], sec, ck.to_device(ct))
+    refreshes = plan(groups, 1 << 40, L, n).refreshes
+    assert refreshes >= 2
+    s, s_ntt, draws, draws_dev, ct = secret_inputs(ck, ctx, d, 504, refreshes)
+    p, got = run(ck, ctx, groups, 1 << 40, [ck.to_device(w) for w in W], s_ntt, draws_dev, ck.to_device(ct))
     cur = ct.astype(np.uint64)
+    it = iter(draws)
     for step, w in zip(p.steps, W):
         lv = step.level
         pt = OE.encode_poly(w.reshape(d, d, n // 2), SCALE, qs[:lv], psis[:lv], LOG_N)
         mac = OL.mac_poly(pt, cur, qs[:lv])
         cur = OL.rescale(mac, qs[:lv], psis[:lv], LOG_N)
         if step.refresh_after:
+            a, e = next(it)
             cur = OR.refresh(cur, s, a, e, qs, psis, LOG_N, L)
     assert got.shape == cur.shape
     assert np.array_equal(got, cur.astype(np.uint32))
@@ -105,15 +132,14 @@ def test_chain_at_the_benchmarked_width(gpu_lib):
     s_res = np.stack([np.mod(s, q) for q in qs]).astype(np.uint32)
     s_ntt = ck.to_device(s_res)
     ck.ckks_ntt(ctx, s_ntt, 1, L)
-    a = gen.uniform_residues(st["residues"], (d,), qs, n)
-    e = gen.gaussian_error(st["error"], (d, n)).astype(np.int32)
-    ct = gen.uniform_residues(st["residues"], (d, 2), qs, n)
-    sec = {"s_ntt": s_ntt, "a": ck.to_device(a), "e": ck.to_device(e)}
     budget = plan(groups, 1 << 40, L, n).steps[0].encoded_bytes           # only the first group fits
     p = plan(groups, budget, L, n)
     assert [st_.pinned for st_ in p.steps] == [True, False, False]
-    ex = Executor(ctx, p, [ck.to_device(w) for w in W], SCALE, sec)
-    out, limbs = ex.run(ck.to_device(ct))
+    draws = [(gen.uniform_residues(st["residues"], (d,), qs, n), gen.gaussian_error(st["error"], (d, n)).astype(np.int32))
+             for _ in range(p.refreshes)]
+    ct = gen.uniform_residues(st["residues"], (d, 2), qs, n)
+    ex = Executor(ctx, p, [ck.to_device(w) for w in W], SCALE, s_ntt)
+    out, limbs = ex.run(ck.to_device(ct), [(ck.to_device(a), ck.to_device(e)) for a, e in draws])
     got = ck.to_host_u32(out[: d * 2 * limbs * n]).reshape(d, 2, limbs, n)
     cur = ct.astype(np.uint64)
     for step, c in zip(p.steps, consts):
@@ -122,5 +148,6 @@ def test_chain_at_the_benchmarked_width(gpu_lib):
         pt = np.broadcast_to(w_enc[..., None], (d, d, lv, n))
         cur = OL.rescale(OL.mac_poly(pt, cur, qs[:lv]), qs[:lv], psis[:lv], log_n)
         if step.refresh_after:
+            a, e = draws[sum(x.refresh_after for x in p.steps[: p.steps.index(step)])]
             cur = OR.refresh(cur, s, a, e, qs, psis, log_n, L)
     assert np.array_equal(got, cur.astype(np.uint32))

@@ -261,30 +261,76 @@ def test_tiled_product_decodes_to_w_times_x():
         assert np.max(np.abs(got - bsgs.replicate(y[i * d:(i + 1) * d], slots))) < 1e-3
 
 
-def test_lazy_giant_sum_matches_the_sum_of_rotations():
-    """The product's giant steps (summed before one division by P) decrypt to the sum of
-    the individually rotated inner sums within the rounding of the divisions: at most
-    n2 - 1 ModDown roundings before the closing rescale, which divides them away, so the
-    two decryptions differ by the closing rescale's own rounding terms only."""
-    from oracle import linear as OL
-    log_n, L, d, n1 = 6, 3, 16, 4
+def _dec_diff(a, b, s, qs, psis, log_n):
+    """Centred coefficients of dec(a) - dec(b) mod Q (both (2, L, N) NTT form)."""
+    Q = 1
+    for q in qs:
+        Q *= q
+    da = rlwe.decrypt(a, s, qs, psis, log_n)
+    db = rlwe.decrypt(b, s, qs, psis, log_n)
+    out = []
+    for x, y in zip(da, db):
+        v = (int(x) - int(y)) % Q
+        out.append(v - Q if v > Q // 2 else v)
+    return out
+
+
+@pytest.mark.parametrize("log_n,L,d,n1,seed", [(6, 3, 16, 4, 95), (7, 3, 32, 4, 96), (6, 4, 16, 2, 97)])
+def test_lazy_schedule_within_the_bound_of_the_eager_product(log_n, L, d, n1, seed):
+    """matvec (every giant-step rotation divided by P on its own, the plain formula)
+    and matvec_lazy (giant steps summed before one division by P) on uniform residues.
+    Before the closing rescale the sums differ (the roundings are not the same) and
+    their decryptions by at most (n2 / 2)(N + 1) per coefficient; after it, by at most
+    eager_lazy_bound (N + 1).  A misplaced giant-step term leaves a difference spread
+    over all of Z_Q."""
     n2 = d // n1
-    n, qs_p, psis_p, s, st = _chain(log_n, L, 95)
+    n, qs_p, psis_p, s, st = _chain(log_n, L, seed)
     qs, psis = qs_p[:L], psis_p[:L]
     pt = gen.uniform_residues(st["residues"], (n2, n1), qs, n)
     ct = gen.uniform_residues(st["residues"], (2,), qs, n)
     keys = {r: KS.rotation_key(s, r, gen.uniform_residues(st["residues"], (L,), qs_p, n),
                                gen.gaussian_error(st["error"], (L, n)), qs_p, psis_p, log_n)
             for r in list(range(1, n1)) + [j * n1 for j in range(1, n2)]}
-    lazy = bsgs.matvec(pt, ct, n1, keys, qs_p, psis_p, log_n)
-    # eager: every giant-step rotation divided by P on its own, then summed
-    baby = [ct.astype(np.uint64)] + [KS.rotate(ct, i, keys[i], qs_p, psis_p, log_n) for i in range(1, n1)]
-    inner = OL.mac_poly(pt, np.stack(baby), qs)
+    z_e = bsgs.matvec(pt, ct, n1, keys, qs_p, psis_p, log_n, rescaled=False)
+    z_l = bsgs.matvec_lazy(pt, ct, n1, keys, qs_p, psis_p, log_n, rescaled=False)
+    assert not np.array_equal(z_l, z_e)
+    pre = _dec_diff(z_l, z_e, s, qs, psis, log_n)
+    assert 0 < max(abs(v) for v in pre) <= (n2 * (n + 1)) // 2
+    eager = bsgs.matvec(pt, ct, n1, keys, qs_p, psis_p, log_n)
+    lazy = bsgs.matvec_lazy(pt, ct, n1, keys, qs_p, psis_p, log_n)
+    bound = bsgs.eager_lazy_bound(n2, log_n, qs[L - 1])
+    assert bound == n + 1
+    diff = _dec_diff(lazy, eager, s, qs[:L - 1], psis[:L - 1], log_n)
+    assert max(abs(v) for v in diff) <= bound
+    # one giant-step term left out of the lazy sum is far outside the bound
+    keys_wrong = dict(keys)
+    keys_wrong[n1] = keys[1] if n1 > 1 else keys[n1]
+    wrong = bsgs.matvec_lazy(pt, ct, n1, keys_wrong, qs_p, psis_p, log_n)
+    diff_w = _dec_diff(wrong, eager, s, qs[:L - 1], psis[:L - 1], log_n)
+    assert max(abs(v) for v in diff_w) > 1000 * bound
+
+
+def test_eager_product_is_the_composition_of_single_rotations():
+    """matvec equals rotations of the inner sums added one by one, each through
+    keyswitch.rotate (the pinned single rotation), then the pinned rescale."""
+    from oracle import linear as OL
+    log_n, L, d, n1 = 6, 3, 12, 3
+    n2 = d // n1
+    n, qs_p, psis_p, s, st = _chain(log_n, L, 98)
+    qs, psis = qs_p[:L], psis_p[:L]
+    pt = gen.uniform_residues(st["residues"], (n2, n1), qs, n)
+    ct = gen.uniform_residues(st["residues"], (2,), qs, n)
+    keys = {r: KS.rotation_key(s, r, gen.uniform_residues(st["residues"], (L,), qs_p, n),
+                               gen.gaussian_error(st["error"], (L, n)), qs_p, psis_p, log_n)
+            for r in list(range(1, n1)) + [j * n1 for j in range(1, n2)]}
+    got = bsgs.matvec(pt, ct, n1, keys, qs_p, psis_p, log_n)
     q = np.array(qs, dtype=np.uint64)[:, None]
-    acc = inner[0].copy()
-    for j in range(1, n2):
-        acc = (acc + KS.rotate(inner[j], j * n1, keys[j * n1], qs_p, psis_p, log_n)) % q
-    eager = OL.rescale(acc[None], qs, psis[:L], log_n)[0]
-    diff = (np.array(rlwe.decrypt(lazy, s, qs[:L - 1], psis[:L - 1], log_n), dtype=object)
-            - np.array(rlwe.decrypt(eager, s, qs[:L - 1], psis[:L - 1], log_n), dtype=object))
-    assert max(abs(int(x)) for x in diff) <= n                 # |s| rounding terms, well below any real signal
+    acc = np.zeros((2, L, n), dtype=np.uint64)
+    for j in range(n2):
+        y = np.zeros((2, L, n), dtype=np.uint64)
+        for i in range(n1):
+            xi = ct.astype(np.uint64) if i == 0 else KS.rotate(ct, i, keys[i], qs_p, psis_p, log_n)
+            y = (y + (pt[j, i].astype(np.uint64)[None] * xi) % q) % q
+        acc = (acc + (y if j == 0 else KS.rotate(y, j * n1, keys[j * n1], qs_p, psis_p, log_n))) % q
+    want = OL.rescale(acc[None], qs, psis[:L], log_n)[0]
+    assert np.array_equal(got, want)

@@ -63,3 +63,36 @@ def test_shape_mismatch_and_short_chain_are_rejected():
         plan([LinearGroup("a", 8, 8), LinearGroup("b", 8, 4)], 0, full_limbs=4, n=N)
     with pytest.raises(ValueError):
         plan(stack(2), 0, full_limbs=2, n=N)          # no rescale would keep 2 limbs
+
+
+class _FakeTensor:
+    """Stand-in with the two methods the draw check reads (a storage span)."""
+
+    def __init__(self, ptr, nbytes):
+        self.ptr, self.nbytes = ptr, nbytes
+
+    def data_ptr(self):
+        return self.ptr
+
+    def numel(self):
+        return self.nbytes // 4
+
+    def element_size(self):
+        return 4
+
+
+def test_each_refresh_needs_its_own_randomness():
+    """Two refreshes never receive the same (a, e) storage, and a pass with fewer
+    draws than refreshes is refused (no GPU: the check only reads storage spans)."""
+    from paper_2606_17421_amd.planner import check_refresh_draws
+    a0, e0 = _FakeTensor(0x1000, 256), _FakeTensor(0x2000, 64)
+    a1, e1 = _FakeTensor(0x3000, 256), _FakeTensor(0x4000, 64)
+    check_refresh_draws([(a0, e0), (a1, e1)], 2)
+    with pytest.raises(ValueError):
+        check_refresh_draws([(a0, e0)], 2)
+    with pytest.raises(ValueError):
+        check_refresh_draws([(a0, e0), (a0, e1)], 2)                 # a shared
+    with pytest.raises(ValueError):
+        check_refresh_draws([(a0, e0), (a1, _FakeTensor(0x2020, 64))], 2)   # e overlaps partly
+    with pytest.raises(ValueError):
+        check_refresh_draws([(a0, e0), (_FakeTensor(0x2000, 16), e1)], 2)   # a inside the first e
