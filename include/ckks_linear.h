@@ -145,6 +145,26 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc,
                            uint32_t d_in, uint32_t limbs, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/* ckks_linear_mac_scalar without a caller workspace, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, result and errors as
+ * ckks_linear_mac_scalar; the matrix-core kernel's workspace (the weight digit
+ * fragments and per-tile flags, ckks_workspace_bytes(ctx, CKKS_OP_MAC_SCALAR,
+ * d_out, d_in, limbs) bytes) is instead a library-owned device array of
+ * CKKS_NOALLOC_SCRATCH_BYTES (64 MiB) on each GPU the library runs on, held
+ * until the process ends.  The call allocates nothing.  Requests needing more
+ * scratch than that return CKKS_E_WORKSPACE (at N = 2^14 and 4 limbs, up to
+ * about 4096 x 1024 weights).  Every call on one GPU shares that GPU's array,
+ * which keeps the last call's contents: calls that overlap in time on one GPU
+ * (different streams, or different host threads) race and must be serialised
+ * by the caller.  The kernels overwrite every scratch byte they read, so
+ * nothing needs clearing between calls. */
+#define CKKS_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int ckks_linear_mac_scalar_noalloc(const ckks_ctx* ctx, const uint32_t* w_enc,
+                                   const uint32_t* ct_in, uint32_t* ct_out,
+                                   uint32_t d_out, uint32_t d_in, uint32_t limbs,
+                                   void* stream);
+
 /* ct x pt MAC with full-polynomial NTT-form weights (the fallback-encode
  * path of section 4.2): slot-wise
  *     ct_out[j][c][l][k] = sum_i pt[j][i][l][k] * ct_in[i][c][l][k]  mod q_l,

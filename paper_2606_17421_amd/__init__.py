@@ -57,6 +57,7 @@ _SIGS = {
     "ckks_linear_encode_scalar": (_i32, [_vp, _vp, _u32, _u32, _u32, _dbl, _vp, _vp]),
     "ckks_linear_encode_poly": (_i32, [_vp, _vp, _u32, _u32, _dbl, _vp, _vp]),
     "ckks_linear_mac_scalar": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp, _sz, _vp]),
+    "ckks_linear_mac_scalar_noalloc": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp]),
     "ckks_linear_mac_poly": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp]),
     "ckks_rescale": (_i32, [_vp, _vp, _vp, _u32, _u32, _vp, _sz, _vp]),
     "ckks_encrypt": (_i32, [_vp, _vp, _vp, _vp, _vp, _u32, _u32, _vp, _vp]),
@@ -204,6 +205,19 @@ def ckks_linear_mac_scalar(ctx: Context, w_enc, ct_in, ct_out, d_out: int, d_in:
         ctx.handle, _ptr(w_enc, "w_enc", d_out * d_in * limbs * 4, 4),
         _ptr(ct_in, "ct_in", d_in * ct_words * 4, 4), _ptr(ct_out, "ct_out", d_out * ct_words * 4, 4),
         d_out, d_in, limbs, ws, workspace_bytes, _stream(stream)), "ckks_linear_mac_scalar")
+
+
+def ckks_linear_mac_scalar_noalloc(ctx: Context, w_enc, ct_in, ct_out, d_out: int, d_in: int, limbs: int,
+                                   stream=None) -> None:
+    """ckks_linear_mac_scalar with the library's own per-GPU scratch as workspace."""
+    ct_words = 2 * limbs * ctx.n if d_out else 0
+    _check(_lib.ckks_linear_mac_scalar_noalloc(
+        ctx.handle, _ptr(w_enc, "w_enc", d_out * d_in * limbs * 4, 4),
+        _ptr(ct_in, "ct_in", d_in * ct_words * 4, 4), _ptr(ct_out, "ct_out", d_out * ct_words * 4, 4),
+        d_out, d_in, limbs, _stream(stream)), "ckks_linear_mac_scalar_noalloc")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 def ckks_linear_mac_poly(ctx: Context, pt, ct_in, ct_out, d_out: int, d_in: int, limbs: int, stream=None) -> None:

@@ -12,12 +12,16 @@
 
 #include "ckks_internal.hpp"
 
+static_assert(CKKS_NOALLOC_SCRATCH_BYTES == ckks::kNoAllocScratchBytes, "scratch size in the header and the library");
+
 struct ckks_ctx {
   int device = 0;
   uint32_t log_n = 0, n = 0, L = 0;
   std::vector<uint32_t> q, psi;
   int mac_algo = CKKS_MAC_AUTO;
   void* dev = nullptr;
+  void* scratch = nullptr;            // the device's no-allocation MAC workspace (library-owned)
+  hipError_t scratch_status = hipSuccess;
   ckks::Tables t{};
 };
 
@@ -343,6 +347,10 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
     delete c;
     return hip_fail(he == hipSuccess ? hipErrorInvalidDevice : he, "hipDeviceGetAttribute(compute units)");
   }
+  // The no-allocation MAC's workspace: this device's copy of the library's
+  // scratch array, resolved here with the device current.
+  c->scratch_status = ckks::noalloc_scratch(device, &c->scratch);
+  if (c->scratch_status != hipSuccess) c->scratch = nullptr;
   auto* base = static_cast<unsigned char*>(c->dev);
   ckks::Tables& t = c->t;
   t.log_n = log_n;
@@ -478,9 +486,11 @@ static int check_mac_shapes(uint32_t d_out, uint32_t d_in) {
   return CKKS_OK;
 }
 
-int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc, const uint32_t* ct_in,
-                           uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
-                           void* workspace, size_t workspace_bytes, void* stream) {
+// The scalar MAC behind both entry points.  noalloc: the matrix-core workspace
+// is the context device's library-owned scratch array instead of the caller's.
+static int mac_scalar_impl(const ckks_ctx* ctx, const uint32_t* w_enc, const uint32_t* ct_in, uint32_t* ct_out,
+                           uint32_t d_out, uint32_t d_in, uint32_t limbs, void* workspace, size_t workspace_bytes,
+                           void* stream, bool noalloc) {
   if (int rc = check_ctx(ctx)) return rc;
   if (int rc = check_limbs(ctx, limbs, 1)) return rc;
   if (int rc = check_mac_shapes(d_out, d_in)) return rc;
@@ -508,6 +518,16 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc, const uin
   const bool use_mfma = ctx->mac_algo == CKKS_MAC_MFMA || (ctx->mac_algo == CKKS_MAC_AUTO && mfma_ok);
   if (use_mfma) {
     const size_t need = ckks::mac_mfma_workspace_bytes(ctx->n, d_out, d_in, limbs);
+    if (noalloc) {
+      if (!ctx->scratch)
+        return hip_fail(ctx->scratch_status, "no-allocation MAC scratch (hipGetSymbolAddress at context creation)");
+      if (need > ckks::kNoAllocScratchBytes)
+        return fail(CKKS_E_WORKSPACE,
+                    "no-allocation MAC needs %zu bytes of scratch for d_out=%u, d_in=%u, limbs=%u; its array holds %zu",
+                    need, d_out, d_in, limbs, ckks::kNoAllocScratchBytes);
+      workspace = ctx->scratch;
+      workspace_bytes = ckks::kNoAllocScratchBytes;
+    }
     if (!workspace || workspace_bytes < need)
       return fail(CKKS_E_WORKSPACE, "MAC workspace %zu bytes < %zu required", workspace_bytes, need);
     if (!aligned16(workspace)) return fail(CKKS_E_INVALID_ARG, "workspace is not 16-byte aligned");
@@ -519,6 +539,17 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc, const uin
     e = ckks::launch_mac_scalar_valu(ctx->t, w_enc, ct_in, ct_out, d_out, d_in, limbs, s);
   }
   return e == hipSuccess ? ok() : hip_fail(e, "mac_scalar launch");
+}
+
+int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc, const uint32_t* ct_in,
+                           uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  return mac_scalar_impl(ctx, w_enc, ct_in, ct_out, d_out, d_in, limbs, workspace, workspace_bytes, stream, false);
+}
+
+int ckks_linear_mac_scalar_noalloc(const ckks_ctx* ctx, const uint32_t* w_enc, const uint32_t* ct_in,
+                                   uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs, void* stream) {
+  return mac_scalar_impl(ctx, w_enc, ct_in, ct_out, d_out, d_in, limbs, nullptr, 0, stream, true);
 }
 
 int ckks_linear_mac_poly(const ckks_ctx* ctx, const uint32_t* pt, const uint32_t* ct_in,

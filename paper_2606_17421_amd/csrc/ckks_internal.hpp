@@ -13,6 +13,8 @@ constexpr int kMaxLimbs = 16;
 constexpr int kMinLogN = 10;
 constexpr int kMaxLogN = 16;
 constexpr uint32_t kMaxMacDin = 1u << 24;  // largest d_in of the scalar MAC entry point
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;  // per-GPU workspace of the no-allocation MAC
+constexpr int kMaxDevices = 64;
 
 // Per-context device tables.  All arrays live in one device allocation owned
 // by the context; [L][N] arrays are limb-major.
@@ -128,6 +130,9 @@ hipError_t launch_mac_scalar_valu(const Tables& t, const uint32_t* w_enc, const 
                                   hipStream_t s);
 
 size_t mac_mfma_workspace_bytes(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs);
+// Device address, on `device` (which must be current), of the library's
+// kNoAllocScratchBytes array that the no-allocation MAC uses as its workspace.
+hipError_t noalloc_scratch(int device, void** out);
 bool mac_mfma_supported(uint32_t d_in);
 hipError_t launch_mac_scalar_mfma(const Tables& t, const uint32_t* w_enc, const uint32_t* ct_in,
                                   uint32_t* ct_out, uint32_t d_out, uint32_t d_in, uint32_t limbs,

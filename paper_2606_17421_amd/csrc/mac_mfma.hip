@@ -29,7 +29,15 @@
 // XCD-aware grouped order so that the weights of a row group and the columns
 // shared by its row tiles stay in one XCD's L2.  One workgroup-uniform branch
 // per tile selects three or four weight digits.
+#include <mutex>
+
 #include "ckks_internal.hpp"
+
+// Workspace of the no-allocation MAC entry point: one array per GPU, owned by
+// the library for the life of the process.  Its name is a host-side stand-in;
+// kernels receive the device address that hipGetSymbolAddress returns for the
+// current device (see noalloc_scratch below).
+static __device__ __align__(256) unsigned char scratch[ckks::kNoAllocScratchBytes];
 
 namespace ckks {
 namespace {
@@ -322,6 +330,23 @@ Shape shape_of(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
 }
 
 }  // namespace
+
+hipError_t noalloc_scratch(int device, void** out) {
+  // Resolved once per device, with that device current (the caller's guard).
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[device] = p;
+  }
+  *out = addr[device];
+  return hipSuccess;
+}
 
 size_t mac_mfma_workspace_bytes(uint32_t n, uint32_t d_out, uint32_t d_in, uint32_t limbs) {
   if (d_out == 0 || d_in == 0 || d_in > kMaxDin) return 0;
