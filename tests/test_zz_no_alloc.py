@@ -69,3 +69,42 @@ def test_noalloc_mac_refuses_requests_beyond_its_scratch(gpu_lib):
     assert e.value.code == ck.CKKS_E_WORKSPACE
     assert "scratch" in str(e.value)
     ctx.close()
+
+
+def test_noalloc_mac_replays_under_graph_capture(gpu_lib):
+    """The caller the entry point is for: a HIP graph captures the call (it allocates
+    nothing and records no memset) and is replayed three times, with eager work
+    of the program's own between the replays (a workspace MAC on other inputs, the
+    scratch's other user); every replay equals the eager result."""
+    import torch
+    ck = gpu_lib
+    ctx = ck.Context(11, 3)
+    L, n = ctx.limbs, ctx.n
+    w1, c1 = _layer(ck, ctx, 130, 96, 9003)
+    w2, c2 = _layer(ck, ctx, 64, 64, 9004)
+    d_w1, d_c1 = ck.to_device(w1), ck.to_device(c1)
+    d_w2, d_c2 = ck.to_device(w2), ck.to_device(c2)
+    out = ck.empty_u32((130, 2, L, n))
+    eager = ck.empty_u32((130, 2, L, n))
+    ck.ckks_linear_mac_scalar_noalloc(ctx, d_w1, d_c1, eager, 130, 96, L)
+    other = ck.empty_u32((64, 2, L, n))
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        ck.ckks_linear_mac_scalar_noalloc(ctx, d_w1, d_c1, out, 130, 96, L, stream=s)   # warm-up on the stream
+    s.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        ck.ckks_linear_mac_scalar_noalloc(ctx, d_w1, d_c1, out, 130, 96, L, stream=s)
+    for k in range(3):
+        out.fill_(0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {k}"
+        ck.ckks_linear_mac_scalar_noalloc(ctx, d_w2, d_c2, other, 64, 64, L)           # eager use of the scratch
+        torch.cuda.synchronize()
+    assert np.array_equal(ck.to_host_u32(other)[[0, 63]],
+                          OL.mac_scalar(w2, c2, ctx.moduli, rows=[0, 63]).astype(np.uint32))
+    del g
+    ctx.close()
