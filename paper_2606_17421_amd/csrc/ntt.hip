@@ -58,7 +58,8 @@ constexpr int kColLogE = 6;
 constexpr int kColThreads = 256;
 
 template <bool INV>
-__global__ __launch_bounds__(kColThreads) void ntt16_cols_kernel(Tables tb, uint32_t* rows,
+// Two workgroups per CU (two waves per SIMD, at most 256 registers each).
+__global__ __launch_bounds__(kColThreads, 2) void ntt16_cols_kernel(Tables tb, uint32_t* rows,
                                                                  uint32_t limbs, uint32_t gstride) {
   using P = Plan<16, kColLogE>;
   constexpr int kColsPerRow = 1 << (16 - kColLogE);

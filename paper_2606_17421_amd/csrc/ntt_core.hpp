@@ -71,9 +71,13 @@ __device__ __forceinline__ void fwd_group(uint32_t (&v)[1 << LOGE], uint32_t t, 
         const int j1 = j0 | (1 << lb);
         uint32_t U = v[j0];
         U = min(U, U - q2);                               // [0, 2q)
-        const uint32_t V = mul_shoup_lazy(v[j1], wv, wsv, q);  // [0, 2q)
-        v[j0] = U + V;                                    // [0, 4q)
-        v[j1] = U - V + q2;                               // (0, 4q)
+        // The lazy Shoup product V = a w - floor(a ws / 2^32) q lies in [0, 2q);
+        // formed negated (Vn = 2^32 - V), the two outputs take one subtraction
+        // and one three-input addition.
+        const uint32_t a = v[j1];
+        const uint32_t Vn = __umulhi(a, wsv) * q - a * wv;
+        v[j0] = U - Vn;                                   // U + V in [0, 4q)
+        v[j1] = U + Vn + q2;                              // U - V + 2q in (0, 4q)
       }
     }
   }

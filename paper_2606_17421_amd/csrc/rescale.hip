@@ -236,7 +236,8 @@ __global__ __launch_bounds__(kBlkThreads) void rescale16_top_blocks_kernel(Table
   for (int j = 0; j < P::E; ++j) o[P::template pos<0>(t, j)] = v[j];
 }
 
-__global__ __launch_bounds__(kColThreads) void rescale16_cols_kernel(Tables tb, const uint32_t* __restrict__ A,
+// Two workgroups per CU (two waves per SIMD, at most 256 registers each).
+__global__ __launch_bounds__(kColThreads, 2) void rescale16_cols_kernel(Tables tb, const uint32_t* __restrict__ A,
                                                                     uint32_t* __restrict__ B, uint32_t limbs,
                                                                     size_t chunk_words) {
   using P = Plan<16, kColLogE>;
