@@ -153,8 +153,9 @@ int ckks_linear_mac_scalar(const ckks_ctx* ctx, const uint32_t* w_enc,
  * d_out, d_in, limbs) bytes) is instead a library-owned device array of
  * CKKS_NOALLOC_SCRATCH_BYTES (64 MiB) on each GPU the library runs on, held
  * until the process ends.  The call allocates nothing.  Requests needing more
- * scratch than that return CKKS_E_WORKSPACE (at N = 2^14 and 4 limbs, up to
- * about 4096 x 1024 weights).  Every call on one GPU shares that GPU's array,
+ * scratch than that return CKKS_E_WORKSPACE (the fragments take 4 bytes per
+ * weight and limb, rows rounded up to 128 and d_in to 64: at 4 limbs up to
+ * 3968 x 1024 weights, for any N).  Every call on one GPU shares that GPU's array,
  * which keeps the last call's contents: calls that overlap in time on one GPU
  * (different streams, or different host threads) race and must be serialised
  * by the caller.  The kernels overwrite every scratch byte they read, so
