@@ -19,16 +19,21 @@
 // lane order of v_mfma_i32_16x16x64_i8) per 16-row tile and 64-deep k-step,
 // with a flag for tiles that need a fourth digit.
 //
-// Contraction: a 256-thread workgroup computes a 128 (rows) x 32 (columns)
-// tile of one limb; each wave owns 32 rows x 32 columns (2 x 2 MFMA tiles x 6
-// or 7 shift-class accumulators).  Per k-step the workgroup converts the raw
-// residues of its 32 columns (raw buffer loads issued two steps ahead; rows
-// past d_in read as zero through the buffer range check) into digit fragments
-// in an LDS double buffer, and each wave reads its weight fragments from
-// global memory (L2 resident, issued one step ahead).  Workgroups run in an
-// XCD-aware grouped order so that the weights of a row group and the columns
-// shared by its row tiles stay in one XCD's L2.  One workgroup-uniform branch
-// per tile selects three or four weight digits.
+// Every wave owns 32 rows x 32 columns of one limb (2 x 2 MFMA tiles x 6 or
+// 7 shift-class accumulators) and reads its weight fragments from global
+// memory (L2 resident, one k-step ahead).  Two contraction forms:
+//  * column-stationary (d_in <= 1024): a 512-thread workgroup owns 32 columns
+//    and converts all of their residues once into digit fragments for every
+//    k-step, held in LDS (<= 128 KiB, one workgroup per CU); its 8 waves then
+//    walk the row tiles with no further synchronisation.  Each residue is
+//    loaded and converted once per call.
+//  * streamed (1024 < d_in <= 4096): a 256-thread workgroup computes a 128 x
+//    32 tile; per k-step it converts the residues of its 32 columns (loads
+//    issued two steps ahead) into an LDS double buffer and synchronises, two
+//    workgroups per CU; XCD-aware grouped order keeps a row group's weights
+//    and the columns its row tiles share in one XCD's L2.
+// In both, rows past d_in read as zero through the buffer range check, and a
+// wave-uniform branch per tile selects three or four weight digits.
 #include <mutex>
 
 #include "ckks_internal.hpp"
@@ -313,6 +318,150 @@ __global__ __launch_bounds__(kThreads, 2) void mac_mfma_kernel(
     mac_tile<3>(tb, adig_wave, ks_total, bsrc, row_bytes, d_in, bs, out, l, lane);
 }
 
+// Column-stationary contraction (d_in <= kCsMaxDin).  The workgroup converts
+// the residues of its 32 columns for every k-step into LDS, synchronises once,
+// and its 8 waves walk the 32-row wave tiles (wave w takes tiles w, w + 8,
+// ...; at any time the workgroup covers 256 adjacent rows, so workgroups on one
+// XCD moving through the rows together share their weight fragments in L2).
+// Converting the whole column strip once replaces the streamed form's per-tile
+// reload, conversion and per-k-step barrier (1024 -> 6144 at N = 2^16 with 8
+// limbs: 65-68 ms per call against 82-85 ms, bit-identical).
+constexpr uint32_t kCsMaxDin = 1024;
+constexpr int kCsMaxKs = kCsMaxDin / kBK;
+constexpr int kCsThreads = 512;
+constexpr int kCsWaves = kCsThreads / 64;
+
+template <int NDA>
+__device__ __forceinline__ void cs_loop(const v4i* __restrict__ adig_wave, uint32_t ks_total,
+                                        const v4i (*bs)[kFragsPerStep], v4i (&acc)[kMT][kNT][NDA + 3],
+                                        uint32_t lane) {
+  const rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<v4i*>(adig_wave), 0,
+                                                      kMT * ks_total * 4 * 64 * 16, kRsrcWord3);
+  v4i af[2][kMT][NDA];
+  auto load_a = [&](v4i (&a)[kMT][NDA], uint32_t ks) {
+#pragma unroll
+    for (int mt = 0; mt < kMT; ++mt)
+#pragma unroll
+      for (int d = 0; d < NDA; ++d)
+        a[mt][d] = (v4i)__builtin_amdgcn_raw_buffer_load_b128(ra, lane * 16, ((mt * ks_total + ks) * 4 + d) * 1024, 0);
+  };
+  auto step = [&](uint32_t ks, v4i (&a_cur)[kMT][NDA], v4i (&a_nxt)[kMT][NDA]) {
+    load_a(a_nxt, ks + 1 < ks_total ? ks + 1 : ks_total - 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      v4i bf[kNT];
+#pragma unroll
+      for (int nt = 0; nt < kNT; ++nt) bf[nt] = bs[ks][(nt * 4 + b) * 64 + lane];
+#pragma unroll
+      for (int d = 0; d < NDA; ++d)
+#pragma unroll
+        for (int mt = 0; mt < kMT; ++mt)
+#pragma unroll
+          for (int nt = 0; nt < kNT; ++nt)
+            acc[mt][nt][d + b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a_cur[mt][d], bf[nt], acc[mt][nt][d + b], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  load_a(af[0], 0);
+  uint32_t ks = 0;
+  for (; ks + 1 < ks_total; ks += 2) {
+    step(ks, af[0], af[1]);
+    step(ks + 1, af[1], af[0]);
+  }
+  if (ks < ks_total) step(ks, af[0], af[1]);
+}
+
+template <int NDA>
+__device__ __forceinline__ void cs_tile(const Tables& tb, const v4i* __restrict__ adig_wave, uint32_t ks_total,
+                                        const v4i (*bs)[kFragsPerStep], const rsrc_t& out, uint32_t l, uint32_t lane,
+                                        uint32_t row_bytes) {
+  v4i acc[kMT][kNT][NDA + 3];
+#pragma unroll
+  for (int mt = 0; mt < kMT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < kNT; ++nt)
+#pragma unroll
+      for (int s = 0; s < NDA + 3; ++s) acc[mt][nt][s] = v4i{0, 0, 0, 0};
+  cs_loop<NDA>(adig_wave, ks_total, bs, acc, lane);
+  epilogue<NDA>(acc, tb, l, lane, out, row_bytes);
+}
+
+__global__ __launch_bounds__(kCsThreads, 1) void mac_cs_kernel(
+    Tables tb, const v4i* __restrict__ adig, const uint32_t* __restrict__ flags,
+    const uint32_t* __restrict__ ct_in, uint32_t* __restrict__ ct_out, uint32_t d_out, uint32_t d_in,
+    uint32_t limbs, uint32_t mt_total, uint32_t ks_total, uint32_t tiles_n) {
+  __shared__ v4i bs[kCsMaxKs][kFragsPerStep];  // residue digit fragments of every k-step (128 KiB)
+  // Consecutive workgroup ids alternate XCDs: each XCD takes a contiguous range
+  // of (limb, column tile), so the workgroups resident on one XCD share a limb's
+  // weight fragments in its L2.
+  const uint32_t G = gridDim.x;
+  uint32_t lid = blockIdx.x;
+  if ((G & 7u) == 0) lid = (lid & 7u) * (G >> 3) + (lid >> 3);
+  const uint32_t l = lid / tiles_n, ntile = lid - l * tiles_n;
+  const uint32_t n = tb.n;
+  const uint32_t col0 = ntile * kBN;  // column in [0, 2N): component c = col0 / N
+  const uint32_t c = col0 >> tb.log_n, k0 = col0 & (n - 1);
+  const uint32_t row_bytes = 2u * limbs * n * 4u;
+  const uint32_t* bsrc = ct_in + (static_cast<size_t>(c) * limbs + l) * n + k0;
+  const uint32_t row_words = row_bytes >> 2;
+  const uint32_t tid = threadIdx.x;
+
+  // Fill: thread (half h, k group kg, column col) converts 8 consecutive k of
+  // one column for every k-step ks = h, h + 2, ...; all loads are issued first.
+  {
+    const uint32_t col = tid % kBN, kg = (tid / kBN) & 7, h = tid / 256;  // h is wave-uniform
+    const uint32_t frag_lane = (col & 15) + 16 * (kg >> 1), nt_s = col >> 4, half = kg & 1;
+    uint32_t raw[kCsMaxKs / 2][8];
+#pragma unroll
+    for (int i = 0; i < kCsMaxKs / 2; ++i) {
+      const uint32_t ks = 2 * i + h;
+      if (ks < ks_total) {
+        const uint32_t rows = d_in - ks * kBK < kBK ? d_in - ks * kBK : kBK;
+        const rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint32_t*>(bsrc) + static_cast<size_t>(ks) * kBK * row_words, 0, rows * row_bytes, kRsrcWord3);
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+          raw[i][r] = __builtin_amdgcn_raw_buffer_load_b32(rs, (kg * 8 + r) * row_bytes + col * 4, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kCsMaxKs / 2; ++i) {
+      const uint32_t ks = 2 * i + h;
+      if (ks < ks_total) {
+        uint32_t lo[4], hi[4];
+        transpose4(raw[i][0] + kBias, raw[i][1] + kBias, raw[i][2] + kBias, raw[i][3] + kBias, lo);
+        transpose4(raw[i][4] + kBias, raw[i][5] + kBias, raw[i][6] + kBias, raw[i][7] + kBias, hi);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          uint2* dst = reinterpret_cast<uint2*>(&bs[ks][(nt_s * 4 + b) * 64 + frag_lane]) + half;
+          *dst = make_uint2(lo[b] ^ kBias, hi[b] ^ kBias);
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const uint32_t wtiles = (d_out + kMT * 16 - 1) / (kMT * 16);
+  for (uint32_t wt = wave; wt < wtiles; wt += kCsWaves) {
+    const uint32_t mt_wave = wt * kMT;
+    uint32_t top = 0;
+#pragma unroll
+    for (int i = 0; i < kMT; ++i) top |= flags[l * mt_total + mt_wave + i];
+    top = __builtin_amdgcn_readfirstlane(top);
+    const v4i* adig_wave = adig + (static_cast<size_t>(l) * mt_total + mt_wave) * ks_total * 4 * 64;
+    const uint32_t row0 = mt_wave * 16;
+    const uint32_t rows = d_out - row0 < kMT * 16 ? d_out - row0 : kMT * 16;
+    uint32_t* dst = ct_out + ((static_cast<size_t>(row0) * 2 + c) * limbs + l) * n + k0;
+    const rsrc_t out = __builtin_amdgcn_make_buffer_rsrc(dst, 0, rows * row_bytes, kRsrcWord3);
+    if (top != 0)
+      cs_tile<4>(tb, adig_wave, ks_total, bs, out, l, lane, row_bytes);
+    else
+      cs_tile<3>(tb, adig_wave, ks_total, bs, out, l, lane, row_bytes);
+  }
+}
+
 struct Shape {
   uint32_t tiles_m, tiles_n, mt_total, ks_total;
   size_t adig_bytes, flag_bytes;
@@ -367,6 +516,13 @@ hipError_t launch_mac_scalar_mfma(const Tables& t, const uint32_t* w_enc, const 
                                                                  s.ks_total, adig, flags);
   const size_t grid = static_cast<size_t>(limbs) * s.tiles_n * s.tiles_m;
   if (grid >= (size_t(1) << 31)) return hipErrorInvalidValue;  // tile indices are 32-bit
+  if (d_in <= kCsMaxDin) {
+    const size_t cgrid = static_cast<size_t>(limbs) * s.tiles_n;
+    if (cgrid >= (size_t(1) << 31)) return hipErrorInvalidValue;
+    mac_cs_kernel<<<static_cast<uint32_t>(cgrid), kCsThreads, 0, st>>>(t, adig, flags, ct_in, ct_out, d_out, d_in,
+                                                                      limbs, s.mt_total, s.ks_total, s.tiles_n);
+    return hipGetLastError();
+  }
   mac_mfma_kernel<<<static_cast<uint32_t>(grid), kThreads, 0, st>>>(t, adig, flags, ct_in, ct_out, d_out, d_in, limbs,
                                                                    s.mt_total, s.ks_total, s.tiles_m, s.tiles_n);
   return hipGetLastError();

@@ -1,7 +1,9 @@
 """GPU parity at the edges of the kernels' tilings and arithmetic bounds.
 
 * The matrix-core MAC over several row, column and k tiles with ragged tails
-  in every dimension, and at the largest d_in its exact epilogue allows
+  in every dimension, on both sides of the d_in at which its contraction
+  changes form, with three- and four-digit weight tiles mixed, and at the
+  largest d_in its exact epilogue allows
   (4096), with operands that make the shift-class sums as large as valid
   residues can; one past that limit the library refuses the matrix-core path
   and its automatic choice takes the VALU kernel.
@@ -57,6 +59,29 @@ def test_mac_scalar_multitile_ragged(gpu_lib, algo):
     w = np.stack([rng.integers(0, q, (d_out, d_in), dtype=np.uint64) for q in qs], -1).astype(np.uint32)
     ct = residues(4243, (d_in, 2), qs, n)
     got = run_mac(ck, ctx, w, ct, d_out, d_in, limbs, ck.CKKS_MAC_VALU if algo == "valu" else ck.CKKS_MAC_MFMA)
+    assert np.array_equal(got, OL.mac_scalar(w, ct, qs).astype(np.uint32))
+
+
+@pytest.mark.parametrize("d_in,d_out", [(1024, 300), (1025, 150)])
+def test_mac_mfma_both_contraction_forms(gpu_lib, d_in, d_out):
+    """d_in = 1024 is the largest the column-stationary contraction takes (16
+    k-steps held in LDS; 10 wave tiles of 32 rows, so two of the 8 waves take a
+    second one, the last 12 rows deep); d_in = 1025 the smallest the streamed
+    contraction takes (17 k-steps, the last one row deep).  The 32-row wave
+    tiles alternate between small centred weights (three digits) and general
+    residues (four digits)."""
+    ck = gpu_lib
+    log_n, limbs = 10, 2
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, n = ctx.moduli, ctx.n
+    rng = np.random.default_rng(d_in * 7 + d_out)
+    small = rng.integers(-0x7F7F7F, 0x7F7F7F + 1, (d_out, d_in), dtype=np.int64)
+    w = np.stack([np.mod(small, q) for q in qs], -1).astype(np.uint32)
+    general = np.stack([rng.integers(0, q, (d_out, d_in), dtype=np.uint64) for q in qs], -1).astype(np.uint32)
+    odd_tile = (np.arange(d_out) // 32) % 2 == 1
+    w[odd_tile] = general[odd_tile]
+    ct = residues(d_in + 1, (d_in, 2), qs, n)
+    got = run_mac(ck, ctx, w, ct, d_out, d_in, limbs, ck.CKKS_MAC_MFMA)
     assert np.array_equal(got, OL.mac_scalar(w, ct, qs).astype(np.uint32))
 
 
