@@ -61,8 +61,9 @@ __global__ __launch_bounds__(kThreads) void mac_scalar_valu_kernel(
 // outputs j0 .. j0 + kPolyRows - 1, with 16-byte loads.  Each ciphertext
 // residue quad is loaded once per kPolyRows outputs; every plaintext residue
 // is read exactly once.  Workgroups with the same (l, slot block) and
-// consecutive row groups are adjacent in launch order, so the shared
-// ciphertext columns are served from L2.  Four rows per thread when the grid
+// consecutive row groups are adjacent in logical order, and each XCD runs a
+// contiguous range of logical ids, so the shared ciphertext columns are
+// fetched once into that XCD's L2.  Four rows per thread when the grid
 // still holds at least 8 workgroups per CU; narrower layers (the 32-output
 // groups of a decode stack or a BSGS giant-step set) take two rows per thread
 // for twice the workgroups: 47.7 -> 32.2 us at 32 x 32, 4 limbs, N = 2^13
@@ -77,8 +78,13 @@ __global__ __launch_bounds__(kThreads) void mac_poly_kernel(
   const uint32_t groups = (d_out + kPolyRows - 1) / kPolyRows;
   const uint32_t blocks_per_row = n / (kThreads * kPolySlots);
   // blockIdx.x = (l * blocks_per_row + kb) * groups + g
-  const uint32_t g = blockIdx.x % groups;
-  const uint32_t lk = blockIdx.x / groups;
+  // Consecutive workgroup ids alternate XCDs: each XCD takes a contiguous
+  // range of logical ids, so the row groups sharing a column block meet in one L2.
+  const uint32_t G = gridDim.x;
+  uint32_t lid = blockIdx.x;
+  if ((G & 7u) == 0) lid = (lid & 7u) * (G >> 3) + (lid >> 3);
+  const uint32_t g = lid % groups;
+  const uint32_t lk = lid / groups;
   const uint32_t l = lk / blocks_per_row;
   const uint32_t k = ((lk % blocks_per_row) * kThreads + threadIdx.x) * kPolySlots;
   const uint32_t j0 = g * kPolyRows;
