@@ -63,6 +63,49 @@ def test_ntt_and_intt_bit_exact(gpu_lib, log_n):
         assert np.array_equal(got[:, l], ON.intt(a[:, l].astype(np.uint64), qs[l], ctx.roots[l], log_n))
 
 
+def test_longest_chain_16_limbs(gpu_lib):
+    """The longest modulus chain the context accepts (16 limbs), at N = 2^10:
+    the chain and roots, the transforms, scalar encode, both scalar MAC kernels
+    and the poly MAC, each against the oracle."""
+    ck = gpu_lib
+    log_n, limbs = 10, 16
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, n = ctx.moduli, 1 << log_n
+    assert qs == OP.moduli(log_n, limbs)
+    assert ctx.roots == tuple(OP.psi(q, log_n) for q in qs)
+    a = rand_residues(161, (2,), qs, n)
+    d = ck.to_device(a)
+    ck.ckks_ntt(ctx, d, 2, limbs)
+    got = ck.to_host_u32(d).reshape(a.shape)
+    for l in range(limbs):
+        assert np.array_equal(got[:, l], ON.ntt(a[:, l].astype(np.uint64), qs[l], ctx.roots[l], log_n)), l
+    ck.ckks_intt(ctx, d, 2, limbs)
+    assert np.array_equal(ck.to_host_u32(d).reshape(a.shape), a)
+    rng = np.random.default_rng(162)
+    w = rng.normal(0, 0.02, (40, 37))
+    w_enc = ck.empty_u32((40, 37, limbs))
+    ck.ckks_linear_encode_scalar(ctx, ck.to_device(w), 40, 37, limbs, 2.0**28, w_enc)
+    want_w = OE.encode_scalar(w, 2.0**28, qs).astype(np.uint32)
+    assert np.array_equal(ck.to_host_u32(w_enc), want_w)
+    ct = rand_residues(163, (37, 2), qs, n)
+    want = OL.mac_scalar(want_w, ct, qs).astype(np.uint32)
+    for algo in (ck.CKKS_MAC_VALU, ck.CKKS_MAC_MFMA):
+        ck.ckks_ctx_set_mac_algo(ctx, algo)
+        try:
+            ws_bytes = ck.ckks_workspace_bytes(ctx, ck.CKKS_OP_MAC_SCALAR, 40, 37, limbs)
+            ws = ck.empty_u32((max(ws_bytes, 16) // 4 + 4,))
+            out = ck.empty_u32((40, 2, limbs, n))
+            ck.ckks_linear_mac_scalar(ctx, w_enc, ck.to_device(ct), out, 40, 37, limbs, ws)
+            assert np.array_equal(ck.to_host_u32(out), want), algo
+        finally:
+            ck.ckks_ctx_set_mac_algo(ctx, ck.CKKS_MAC_AUTO)
+    pt = rand_residues(164, (5, 4), qs, n)
+    ct2 = rand_residues(165, (4, 2), qs, n)
+    out = ck.empty_u32((5, 2, limbs, n))
+    ck.ckks_linear_mac_poly(ctx, ck.to_device(pt), ck.to_device(ct2), out, 5, 4, limbs)
+    assert np.array_equal(ck.to_host_u32(out), OL.mac_poly(pt, ct2, qs).astype(np.uint32))
+
+
 def test_ntt_limb_subset_and_empty(gpu_lib):
     ck = gpu_lib
     ctx = ctx_for(ck, 12, 4)
