@@ -40,6 +40,43 @@ __device__ __forceinline__ uint32_t reduce_i64(int64_t x, uint32_t q, double qr)
   return (x < 0 && r != 0) ? q - r : r;
 }
 
+// floor(w 2^32 / q) for w < q (the Shoup companion of w): the fp64 estimate is
+// within one of it, and one remainder check fixes it.
+__device__ __forceinline__ uint32_t shoup_const(uint32_t w, uint32_t q, double qr) {
+  uint32_t ws = static_cast<uint32_t>(static_cast<double>(w) * 4294967296.0 * qr);
+  const int64_t r = static_cast<int64_t>((static_cast<uint64_t>(w) << 32) - static_cast<uint64_t>(ws) * q);
+  if (r < 0) --ws;
+  else if (r >= static_cast<int64_t>(q)) ++ws;
+  return ws;
+}
+
+// (x0 + q0 k - [neg] q0 q1 + e) mod q_l, the refreshed residue of one
+// coefficient: x0 < q0 and k < q1 are the CRT digits, neg the centring flag,
+// e in [-19, 19] the fresh error.  With ka = k + [neg](2 q - q1) (< 2^32; 2 q >
+// q1) the centring folds into the product q0 ka = q0 k - [neg] q0 q1 (mod q);
+// the lazy Shoup product lies in [0, 2q), so x0 mod q + product + e + q lies
+// in [q - 19, 4q + 19) < 2^32 and three conditional subtractions finish.
+struct LiftConst {
+  uint32_t q, q0l, q0ls, d2;
+};
+__device__ __forceinline__ LiftConst lift_const(uint32_t q0, uint32_t q1, uint32_t q, double qr) {
+  LiftConst c;
+  c.q = q;
+  c.q0l = q0 >= q ? q0 - q : q0;  // q0 < 2q
+  c.q0ls = shoup_const(c.q0l, q, qr);
+  c.d2 = 2 * q - q1;
+  return c;
+}
+__device__ __forceinline__ uint32_t lift_residue(const LiftConst& c, uint32_t x0, uint32_t k, bool neg, int32_t e) {
+  const uint32_t ka = neg ? k + c.d2 : k;
+  const uint32_t p = mul_shoup_lazy(ka, c.q0l, c.q0ls, c.q);
+  const uint32_t x0l = min(x0, x0 - c.q);
+  uint32_t t = x0l + p + static_cast<uint32_t>(e + static_cast<int32_t>(c.q));
+  t = min(t, t - 2 * c.q);
+  t = min(t, t - c.q);
+  return min(t, t - c.q);
+}
+
 // Buffer resource over one row of N words (row bases live in scalar
 // registers; per-lane offsets and per-element constants index into it).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* base, uint32_t n) {
@@ -238,16 +275,12 @@ __global__ __launch_bounds__(RefreshPlan<LOGN>::P::T, RefreshPlan<LOGN>::kWavesP
   {
     const uint32_t l = blockIdx.y;
     const uint32_t q = tb.q[l], mu = tb.barrett[l];
-    const uint32_t q0l = q0 >= q ? q0 - q : q0, q1l = q1 >= q ? q1 - q : q1;  // q0, q1 < 2q
-    const uint32_t q2l = mul_mod_barrett(q0l, q1l, q, mu);                      // q0 q1 mod q
+    const LiftConst lc = lift_const(q0, q1, q, tb.q_recip[l]);
 #pragma unroll
     for (int j = 0; j < P::E; ++j) {
-      const uint32_t x0l = x0[j] >= q ? x0[j] - q : x0[j];
-      uint32_t y = add_mod(x0l, mul_mod_barrett(kf[j] & 0x7fffffffu, q0l, q, mu), q);
-      if (kf[j] >> 31) y = sub_mod(y, q2l, q);
       const int32_t ev = static_cast<int32_t>(
           __builtin_amdgcn_raw_buffer_load_b32(er, t * 4, P::template pos<0>(0, j) * 4, 0));
-      v[j] = ev < 0 ? sub_mod(y, static_cast<uint32_t>(-ev), q) : add_mod(y, static_cast<uint32_t>(ev), q);
+      v[j] = lift_residue(lc, x0[j], kf[j] & 0x7fffffffu, (kf[j] >> 31) != 0, ev);
     }
     const size_t tl = static_cast<size_t>(l) << LOGN;
     fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
@@ -320,45 +353,63 @@ __global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPe
   if ((G & 7u) == 0) lid = (lid & 7u) * (G >> 3) + (lid >> 3);
   const size_t c = lid / limbs_out;
   const uint32_t l = lid % limbs_out, t = threadIdx.x;
-  const uint32_t* r0 = ct_out + ((c * 2 + 1) * limbs_out) * N;   // scratch: coefficient residues mod q0, q1
-  const uint32_t* r1 = r0 + N;
-  const int32_t* er = e + c * N;
+  // scratch rows: coefficient residues mod q0, q1; element j of thread t of the
+  // group-0 layout sits at t + T j (buffer loads: the offset j T is a constant)
+  const auto rr0 = row_rsrc(ct_out + ((c * 2 + 1) * limbs_out) * N, N);
+  const auto rr1 = row_rsrc(ct_out + ((c * 2 + 1) * limbs_out + 1) * N, N);
+  const auto rer = row_rsrc(e + c * N, N);
   const uint32_t q0 = tb.q[0], q1 = tb.q[1];
   const uint32_t w = tb.qinv[0 * tb.L + 1], ws = tb.qinv_shoup[0 * tb.L + 1];  // q0^-1 mod q1
   const uint64_t half = static_cast<uint64_t>(q0) * q1 / 2;
   const uint32_t q = tb.q[l], mu = tb.barrett[l];
-  const uint32_t q0l = q0 >= q ? q0 - q : q0, q1l = q1 >= q ? q1 - q : q1;  // q0, q1 < 2q
-  const uint32_t q2l = mul_mod_barrett(q0l, q1l, q, mu);                      // q0 q1 mod q
+  const LiftConst lc = lift_const(q0, q1, q, tb.q_recip[l]);
   uint32_t v[P::E];
   // keeps the element loads below the per-limb constants: scheduled above them,
   // the loads' live ranges spill registers
   __builtin_amdgcn_sched_barrier(0);
+  // loads in batches of 8 elements, each batch issued before the previous one is
+  // used (group 0: element j of thread t at t + T j)
+  constexpr int kB = 8;
+  uint32_t xa[2][kB], xb[2][kB];
+  int32_t ea[2][kB];
+  auto load = [&](int set, int j0) {
 #pragma unroll
-  for (int j = 0; j < P::E; ++j) {
-    const uint32_t idx = P::template pos<0>(t, j);
-    const uint32_t x0 = r0[idx];
-    const uint32_t r0m = x0 >= q1 ? x0 - q1 : x0;                            // x0 < q0 < 2 q1
-    const uint32_t k = mul_shoup(sub_mod(r1[idx], r0m, q1), w, ws, q1);
-    const bool neg = static_cast<uint64_t>(x0) + static_cast<uint64_t>(q0) * k > half;
-    const uint32_t x0l = x0 >= q ? x0 - q : x0;
-    uint32_t y = add_mod(x0l, mul_mod_barrett(k, q0l, q, mu), q);
-    if (neg) y = sub_mod(y, q2l, q);
-    const int32_t ev = er[idx];
-    v[j] = ev < 0 ? sub_mod(y, static_cast<uint32_t>(-ev), q) : add_mod(y, static_cast<uint32_t>(ev), q);
+    for (int i = 0; i < kB; ++i) {
+      const uint32_t jo = P::template pos<0>(0, j0 + i) * 4;
+      xa[set][i] = __builtin_amdgcn_raw_buffer_load_b32(rr0, t * 4, jo, 0);
+      xb[set][i] = __builtin_amdgcn_raw_buffer_load_b32(rr1, t * 4, jo, 0);
+      ea[set][i] = static_cast<int32_t>(__builtin_amdgcn_raw_buffer_load_b32(rer, t * 4, jo, 0));
+    }
+  };
+  load(0, 0);
+#pragma unroll
+  for (int j0 = 0; j0 < P::E; j0 += kB) {
+    const int cur = (j0 / kB) & 1;
+    if (j0 + kB < P::E) load(cur ^ 1, j0 + kB);
+#pragma unroll
+    for (int i = 0; i < kB; ++i) {
+      const uint32_t x0 = xa[cur][i];
+      const uint32_t r0m = x0 >= q1 ? x0 - q1 : x0;                          // x0 < q0 < 2 q1
+      const uint32_t k = mul_shoup(sub_mod(xb[cur][i], r0m, q1), w, ws, q1);
+      const bool neg = static_cast<uint64_t>(x0) + static_cast<uint64_t>(q0) * k > half;
+      v[j0 + i] = lift_residue(lc, x0, k, neg, ea[cur][i]);
+    }
   }
   const size_t tl = static_cast<size_t>(l) << LOGN;
   fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
   wave_relayout<LOGN, LOGE, false>(v, t, lds);
-  const uint32_t cb = pos_coalesced<LOGE>(t, 0);
-  const uint32_t* av = a + (c * limbs_out + l) * N + cb;
-  const uint32_t* sv = s_ntt + static_cast<size_t>(l) * N + cb;
-  uint32_t* o = ct_out + ((c * 2) * limbs_out + l) * N + cb;
-  uint32_t* o1 = o + static_cast<size_t>(limbs_out) * N;       // c1 row l (rows 0, 1 are the scratch)
+  __builtin_amdgcn_sched_barrier(0);  // the combine's loads stay after the transform
+  const uint32_t vofs = pos_coalesced<LOGE>(t, 0) * 4;
+  const auto ra = row_rsrc(a + (c * limbs_out + l) * N, N);
+  const auto rs = row_rsrc(s_ntt + static_cast<size_t>(l) * N, N);
+  const auto ro = row_rsrc(ct_out + ((c * 2) * limbs_out + l) * N, N);
+  const auto ro1 = row_rsrc(ct_out + ((c * 2 + 1) * limbs_out + l) * N, N);  // c1 row l (rows 0, 1 are the scratch)
 #pragma unroll
   for (int j = 0; j < P::E; ++j) {
-    const uint32_t ax = av[j << 6];
-    o[j << 6] = sub_mod(v[j], mul_mod_barrett(ax, sv[j << 6], q, mu), q);
-    if (l >= 2) o1[j << 6] = ax;
+    const uint32_t ax = __builtin_amdgcn_raw_buffer_load_b32(ra, vofs, j << 8, 0);
+    const uint32_t sx = __builtin_amdgcn_raw_buffer_load_b32(rs, vofs, j << 8, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(sub_mod(v[j], mul_mod_barrett(ax, sx, q, mu), q), ro, vofs, j << 8, 0);
+    if (l >= 2) __builtin_amdgcn_raw_buffer_store_b32(ax, ro1, vofs, j << 8, 0);
   }
 }
 
