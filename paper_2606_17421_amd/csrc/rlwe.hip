@@ -320,13 +320,19 @@ __global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPe
   const size_t c = blockIdx.x >> 1;
   const uint32_t l = blockIdx.x & 1, t = threadIdx.x;
   const uint32_t q = tb.q[l], mu = tb.barrett[l];
-  const uint32_t cb = pos_coalesced<LOGE>(t, 0);
-  const uint32_t* c0 = ct_in + ((c * 2) * limbs_in + l) * N + cb;
-  const uint32_t* c1 = c0 + static_cast<size_t>(limbs_in) * N;
-  const uint32_t* sv = s_ntt + static_cast<size_t>(l) * N + cb;
-  uint32_t v[P::E];
+  const uint32_t vofs = pos_coalesced<LOGE>(t, 0) * 4;
+  const auto r_c0 = row_rsrc(ct_in + ((c * 2) * limbs_in + l) * N, N);
+  const auto r_c1 = row_rsrc(ct_in + ((c * 2 + 1) * limbs_in + l) * N, N);
+  const auto r_s = row_rsrc(s_ntt + static_cast<size_t>(l) * N, N);
+  uint32_t v[P::E], xb[P::E], xs[P::E];
 #pragma unroll
-  for (int j = 0; j < P::E; ++j) v[j] = add_mod(c0[j << 6], mul_mod_barrett(c1[j << 6], sv[j << 6], q, mu), q);
+  for (int j = 0; j < P::E; ++j) {
+    v[j] = __builtin_amdgcn_raw_buffer_load_b32(r_c0, vofs, j << 8, 0);
+    xb[j] = __builtin_amdgcn_raw_buffer_load_b32(r_c1, vofs, j << 8, 0);
+    xs[j] = __builtin_amdgcn_raw_buffer_load_b32(r_s, vofs, j << 8, 0);
+  }
+#pragma unroll
+  for (int j = 0; j < P::E; ++j) v[j] = add_mod(v[j], mul_mod_barrett(xb[j], xs[j], q, mu), q);
   wave_relayout<LOGN, LOGE, true>(v, t, lds);
   const size_t tl = static_cast<size_t>(l) << LOGN;
   inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + tl, tb.inv_shoup + tl, q, lds);
@@ -404,12 +410,26 @@ __global__ __launch_bounds__((WholePlan<LOGN>::P::T), (WholePlan<LOGN>::kWavesPe
   const auto rs = row_rsrc(s_ntt + static_cast<size_t>(l) * N, N);
   const auto ro = row_rsrc(ct_out + ((c * 2) * limbs_out + l) * N, N);
   const auto ro1 = row_rsrc(ct_out + ((c * 2 + 1) * limbs_out + l) * N, N);  // c1 row l (rows 0, 1 are the scratch)
+  uint32_t ya[2][kB], ys[2][kB];
+  auto load_as = [&](int set, int j0) {
 #pragma unroll
-  for (int j = 0; j < P::E; ++j) {
-    const uint32_t ax = __builtin_amdgcn_raw_buffer_load_b32(ra, vofs, j << 8, 0);
-    const uint32_t sx = __builtin_amdgcn_raw_buffer_load_b32(rs, vofs, j << 8, 0);
-    __builtin_amdgcn_raw_buffer_store_b32(sub_mod(v[j], mul_mod_barrett(ax, sx, q, mu), q), ro, vofs, j << 8, 0);
-    if (l >= 2) __builtin_amdgcn_raw_buffer_store_b32(ax, ro1, vofs, j << 8, 0);
+    for (int i = 0; i < kB; ++i) {
+      ya[set][i] = __builtin_amdgcn_raw_buffer_load_b32(ra, vofs, (j0 + i) << 8, 0);
+      ys[set][i] = __builtin_amdgcn_raw_buffer_load_b32(rs, vofs, (j0 + i) << 8, 0);
+    }
+  };
+  load_as(0, 0);
+#pragma unroll
+  for (int j0 = 0; j0 < P::E; j0 += kB) {
+    const int cur = (j0 / kB) & 1;
+    if (j0 + kB < P::E) load_as(cur ^ 1, j0 + kB);
+#pragma unroll
+    for (int i = 0; i < kB; ++i) {
+      const uint32_t ax = ya[cur][i];
+      __builtin_amdgcn_raw_buffer_store_b32(sub_mod(v[j0 + i], mul_mod_barrett(ax, ys[cur][i], q, mu), q), ro, vofs,
+                                            (j0 + i) << 8, 0);
+      if (l >= 2) __builtin_amdgcn_raw_buffer_store_b32(ax, ro1, vofs, (j0 + i) << 8, 0);
+    }
   }
 }
 
