@@ -14,9 +14,9 @@
 // Encryption and decryption run the batched NTT kernels over the c0 rows (or
 // the output rows) through their row-group stride, with pointwise passes
 // around them, 16 bytes per thread and limb.  The refresh, up to N = 2^14, is
-// one fused kernel split by output limb for decode-size counts and two
-// transform kernels (decrypt + inverse, lift + forward + combine) for larger
-// ones; above 2^14 it is the pass structure of encryption and decryption.
+// two transform kernels (decrypt + inverse, lift + forward + combine), or up to
+// 2^13 for decode-size counts one fused kernel split by output limb; above
+// 2^14 it is the pass structure of encryption and decryption.
 #include "ntt_core.hpp"
 
 namespace ckks {
@@ -201,8 +201,8 @@ __global__ __launch_bounds__(kThreads) void dte_lift_kernel(Tables tb, const int
   }
 }
 
-// Fused refresh for N <= 2^14 and at most half as many ciphertexts as CUs (a
-// decode-size group): one workgroup per ciphertext and output limb.  Limbs 0
+// Fused refresh for N <= 2^13 and at most one workgroup per CU (a decode-size
+// group): one workgroup per ciphertext and output limb.  Limbs 0
 // and 1 of c0 + c1 (.) s are read coalesced and inverse-transformed in LDS;
 // the CRT value over q0 q1 is kept as its two digits x = x0 + q0 k (k with the
 // centring flag in bit 31) in the group-0 layout that the forward transform
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(kThreads) void dte_lift_kernel(Tables tb, const int
 // thread (1024 threads at 2^14) keeps the live state in registers.
 template <int LOGN>
 struct RefreshPlan {
-  static_assert(LOGN <= 14, "the fused refresh serves N <= 2^14");
+  static_assert(LOGN <= 13, "the fused refresh serves N <= 2^13");
   static constexpr int LOGE = 4;
   using P = Plan<LOGN, LOGE>;
   static constexpr int kWavesPerSimd = 4;
@@ -488,11 +488,13 @@ hipError_t launch_decrypt(const Tables& t, const uint32_t* ct, const uint32_t* s
 hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs_in, const uint32_t* s_ntt,
                           const uint32_t* a, const int32_t* e, uint32_t count, uint32_t limbs_out,
                           uint32_t* ct_out, hipStream_t s) {
-  // Up to 2^14: more ciphertexts than half the CUs take the two-kernel route
-  // (768 ciphertexts at 2^14: 0.46 ms against 0.52 ms fused), fewer the fused
-  // kernel split by output limb (32 ciphertexts: the plan step 13.6 ms against
-  // 13.9 ms).
-  if (2 * static_cast<size_t>(count) > t.num_cus) {
+  // Up to 2^13, launches of at most one fused workgroup (ciphertext x output
+  // limb) per CU take the fused kernel split by output limb, whose chain is
+  // three transforms (64 ciphertexts x 4 limbs at 2^13: 26.7 against 30.7 us);
+  // larger ones, and every count at 2^14 (its fused workgroup is 1024
+  // threads), the two-kernel route (32 ciphertexts at 2^14: 40.9 against
+  // 41.8 us; 128: 62.5 against 89.5 us; 768: 0.36 against 0.52 ms).
+  if (t.log_n >= 14 || static_cast<size_t>(count) * limbs_out > t.num_cus) {
     switch (t.log_n) {
       case 10: return launch_refresh_two<10>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
       case 11: return launch_refresh_two<11>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
@@ -507,7 +509,6 @@ hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs
     case 11: return launch_refresh_fused<11>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
     case 12: return launch_refresh_fused<12>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
     case 13: return launch_refresh_fused<13>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
-    case 14: return launch_refresh_fused<14>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
     default: break;
   }
   // N >= 2^15: pointwise passes around the batched transforms (at 2^15 the
