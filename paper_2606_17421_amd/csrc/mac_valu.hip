@@ -67,8 +67,28 @@ __global__ __launch_bounds__(kThreads) void mac_scalar_valu_kernel(
 // still holds at least 8 workgroups per CU; narrower layers (the 32-output
 // groups of a decode stack or a BSGS giant-step set) take two rows per thread
 // for twice the workgroups: 47.7 -> 32.2 us at 32 x 32, 4 limbs, N = 2^13
-// (2.8 -> 4.2 TB/s of plaintext stream).
+// (2.8 -> 4.2 TB/s of plaintext stream).  Per input the row loads are all
+// issued before the first product (a ragged last group re-reads row 0 for its
+// missing rows and discards those sums), so a wave waits on memory once per
+// input instead of once per row: 31.1 -> 24.9 us at 32 x 32, 2^13, 4 limbs.
+// The 4-row kernel (wide layers) loads the plaintexts, which are read once,
+// non-temporally, so that they do not displace the ciphertext columns every
+// row group re-reads from L2: 669 -> 623 us at 64 x 64, 2^15, 6 limbs.  At
+// 32 x 32 the non-temporal loads were slower, so the 2-row kernel keeps plain
+// loads.
 constexpr int kPolySlots = 4;
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool kNonTemporal>
+__device__ __forceinline__ uint4 load_pt(const uint4* p) {
+  if constexpr (kNonTemporal) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+  } else {
+    return *p;
+  }
+}
 
 template <int kPolyRows>
 __global__ __launch_bounds__(kThreads) void mac_poly_kernel(
@@ -106,17 +126,20 @@ __global__ __launch_bounds__(kThreads) void mac_poly_kernel(
     const uint32_t stop = min(d_in, i + kLazy);
     for (; i < stop; ++i) {
       const uint4 x0 = x_ptr[(2ull * i) * ln4], x1 = x_ptr[(2ull * i + 1) * ln4];
+      uint4 pv[kPolyRows];
+#pragma unroll
+      for (int r = 0; r < kPolyRows; ++r) {
+        const uint32_t rr = r < rows ? r : 0;  // rows >= 1; sums of rows past d_out are not stored
+        pv[r] = load_pt<kPolyRows == 4>(&p_ptr[rr * p_row + static_cast<size_t>(i) * ln4]);
+      }
       const uint32_t xs0[4] = {x0.x, x0.y, x0.z, x0.w}, xs1[4] = {x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
       for (int r = 0; r < kPolyRows; ++r) {
-        if (r < rows) {
-          const uint4 pv = p_ptr[r * p_row + static_cast<size_t>(i) * ln4];
-          const uint32_t ps[4] = {pv.x, pv.y, pv.z, pv.w};
+        const uint32_t ps[4] = {pv[r].x, pv[r].y, pv[r].z, pv[r].w};
 #pragma unroll
-          for (int e = 0; e < kPolySlots; ++e) {
-            a0[r][e] += static_cast<uint64_t>(ps[e]) * xs0[e];
-            a1[r][e] += static_cast<uint64_t>(ps[e]) * xs1[e];
-          }
+        for (int e = 0; e < kPolySlots; ++e) {
+          a0[r][e] += static_cast<uint64_t>(ps[e]) * xs0[e];
+          a1[r][e] += static_cast<uint64_t>(ps[e]) * xs1[e];
         }
       }
     }
