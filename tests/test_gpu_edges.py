@@ -157,7 +157,8 @@ def test_rescale_n16_across_staging_chunks(gpu_lib):
 
 
 def test_mac_poly_ragged_row_group(gpu_lib):
-    """7 outputs: one full group of four rows and a ragged group of three."""
+    """7 outputs of a narrow launch (the two-row kernel): three full groups of
+    two rows and a ragged group of one."""
     ck = gpu_lib
     log_n, limbs, d_in, d_out = 11, 2, 6, 7
     ctx = ctx_for(ck, log_n, limbs)
@@ -167,6 +168,25 @@ def test_mac_poly_ragged_row_group(gpu_lib):
     out = ck.empty_u32((d_out, 2, limbs, n))
     ck.ckks_linear_mac_poly(ctx, ck.to_device(pt), ck.to_device(ct), out, d_out, d_in, limbs)
     assert np.array_equal(ck.to_host_u32(out), OL.mac_poly(pt, ct, qs).astype(np.uint32))
+
+
+def test_mac_poly_wide_launch_ragged_row_group(gpu_lib):
+    """87 outputs at N = 2^14, 6 limbs: 22 row groups x 96 (limb, slot block)
+    workgroups fill 8 per CU on 256 CUs, so the four-row kernel runs (its
+    non-temporal plaintext loads); the last group has three rows, and its
+    missing row's loads re-read row 0, whose sums must not be stored."""
+    ck = gpu_lib
+    log_n, limbs, d_in, d_out = 14, 6, 2, 87
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, n = ctx.moduli, ctx.n
+    pt = residues(73, (d_out, d_in), qs, n)
+    ct = residues(74, (d_in, 2), qs, n)
+    out = ck.empty_u32((d_out + 1, 2, limbs, n))
+    out.fill_(-1)  # a guard ciphertext past the last output stays untouched
+    ck.ckks_linear_mac_poly(ctx, ck.to_device(pt), ck.to_device(ct), out, d_out, d_in, limbs)
+    got = ck.to_host_u32(out)
+    assert np.array_equal(got[:d_out], OL.mac_poly(pt, ct, qs).astype(np.uint32))
+    assert np.all(got[d_out] == 0xFFFFFFFF)
 
 
 def _expect_invalid(ck, fn, *args, **kw):
