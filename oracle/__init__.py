@@ -21,7 +21,7 @@ the FHE decode cost-breakdown table of section 6.1):
 * ``poly``    -- schoolbook negacyclic products.
 * ``encode``  -- CKKS canonical-embedding encode/decode by direct O(N^2) sums.
 * ``rlwe``    -- symmetric RLWE encryption / decryption used to make and check
-  the config-1 / config-5 style inputs.
+  the encrypted inputs of the end-to-end checks.
 * ``linear``  -- the modular MAC (scalar and full-polynomial weights) by direct
   modular sums, and rescaling by its CRT closed form.
 

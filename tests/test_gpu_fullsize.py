@@ -112,7 +112,8 @@ def test_scalar_layer_full_size(gpu_lib, key):
 
 
 def test_fallback_layer_full_size(gpu_lib):
-    """Config 5: 64 x 64 full-polynomial weights encoded on the GPU per call, MAC, rescale."""
+    """The full-polynomial layer (64 x 64 slot-vector weights, N = 2^15, 6 limbs, scale
+    2^30) encoded on the GPU per call, MAC, rescale."""
     import torch
     ck = gpu_lib
     cfg = get("c5")
@@ -172,7 +173,7 @@ def test_fallback_layer_full_size(gpu_lib):
 
 
 def test_fallback_encode_every_weight_constant_slots(gpu_lib):
-    """Config 5's shape, every one of its 64 x 64 weights through the full-polynomial
+    """The full-polynomial layer's shape, every one of its 64 x 64 weights through the full-polynomial
     encode on a call of its own: with constant slot vectors (slot value W[j, i]) the
     encoding is the constant polynomial rint(W[j, i] scale), whose NTT is that constant
     in every slot, i.e. exactly the scalar encoding.  So all 4096 plaintexts must equal

@@ -287,7 +287,7 @@ def test_encode_poly_large_coefficients(gpu_lib, log_n, limbs):
     print(f"encode_poly large N=2^{log_n}: {rows_equal} of {2 * limbs} limb rows identical")
 
 
-def test_config1_end_to_end(gpu_lib):
+def test_tiny_layer_end_to_end(gpu_lib):
     """Tiny encrypted layer: GPU encode + MAC + rescale bit-exact, then decrypts to W.x."""
     ck = gpu_lib
     cfg = get("c1")
@@ -316,7 +316,7 @@ def test_config1_end_to_end(gpu_lib):
     assert chk["ok"], chk
 
 
-def test_config5_twin_end_to_end(gpu_lib):
+def test_full_polynomial_twin_end_to_end(gpu_lib):
     """N=2^10, L=3, 8 -> 8 full-polynomial weights encoded on the GPU, MAC, rescale, decrypt."""
     ck = gpu_lib
     cfg = get("c5")

@@ -1,4 +1,4 @@
-"""Config-1 end to end on the oracle alone: encode + encrypt activations, scalar
+"""The tiny 16 -> 16 layer (N = 2^10, 2 limbs) end to end on the oracle alone: encode + encrypt activations, scalar
 weights, MAC, rescale, decrypt, decode, and compare with fp64 W.x within the
 analytic noise bound (rescale rounding dominates: sd ~ 1.6e-4 per slot)."""
 import numpy as np
@@ -8,7 +8,7 @@ from tests.cases import build_layer, check_decrypted
 from workloads import get
 
 
-def test_config1_decrypts_to_w_times_x():
+def test_tiny_layer_decrypts_to_w_times_x():
     cfg = get("c1")
     layer = build_layer(cfg)
     w_enc = encode.encode_scalar(layer.W, cfg.scale, layer.qs)
@@ -21,7 +21,7 @@ def test_config1_decrypts_to_w_times_x():
     assert 0.5 * chk["sd"] < chk["rms_re"]                    # the noise is really there
 
 
-def test_config5_twin_decrypts_to_slotwise_products():
+def test_full_polynomial_twin_decrypts_to_slotwise_products():
     """Full-polynomial weights: out_j = sum_i W[j,i] (.) x_i slot-wise."""
     cfg = get("c5")
     layer = build_layer(cfg, log_n=10, limbs=3, d_in=4, d_out=3)
