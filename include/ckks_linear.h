@@ -118,9 +118,10 @@ int ckks_linear_encode_scalar(const ckks_ctx* ctx, const double* w, uint32_t d_o
  * p_k = rint(scale * m_k), reduced mod each q_l and taken to NTT form.
  *   slots  device fp64 [count][N/2] (real slot values).
  *   pt     device uint32 [count][limbs][N], NTT form; must not overlap slots.
- * Supported for log_n <= 15 (CKKS_E_UNSUPPORTED above).  The spectral
- * transform runs in fp64, so a coefficient whose scaled value lies within
- * about 1e-9 of a rounding tie may differ by one from an exact evaluation. */
+ * Every supported N (at N = 2^16 count x limbs <= 2^31 / 64, else
+ * CKKS_E_INVALID_ARG).  The spectral transform runs in fp64, so a coefficient
+ * whose scaled value lies within about 1e-9 of a rounding tie may differ by
+ * one from an exact evaluation. */
 int ckks_linear_encode_poly(const ckks_ctx* ctx, const double* slots, uint32_t count,
                             uint32_t limbs, double scale, uint32_t* pt, void* stream);
 

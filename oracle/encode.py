@@ -44,25 +44,27 @@ def _trig_tables(log_n: int):
     return np.cos(np.pi * t / n), np.sin(np.pi * t / n)
 
 
-def encode_coeffs(z, log_n: int) -> np.ndarray:
-    """Real coefficients m_k (fp64) of the inverse canonical embedding of slots z (..., N/2)."""
+def encode_coeffs(z, log_n: int, ks=None) -> np.ndarray:
+    """Real coefficients m_k (fp64) of the inverse canonical embedding of slots z (..., N/2),
+    for every k < N, or only for the indices ks (..., len(ks))."""
     n = 1 << log_n
     z = np.asarray(z)
     zr = np.real(z).astype(np.float64).reshape(-1, n // 2)
     zi = np.imag(z).astype(np.float64).reshape(-1, n // 2) if np.iscomplexobj(z) else None
     cos_t, sin_t = _trig_tables(log_n)
     e = slot_exponents(log_n)
-    out = np.empty((zr.shape[0], n), dtype=np.float64)
+    kall = np.arange(n, dtype=np.int64) if ks is None else np.asarray(ks, dtype=np.int64)
+    out = np.empty((zr.shape[0], len(kall)), dtype=np.float64)
     chunk = max(1, (1 << 22) // (n // 2))
-    for k0 in range(0, n, chunk):
-        k = np.arange(k0, min(n, k0 + chunk), dtype=np.int64)
+    for c0 in range(0, len(kall), chunk):
+        k = kall[c0:c0 + chunk]
         t = np.outer(e, k) % (2 * n)                      # (N/2, chunk): exponent of zeta_j^k
         # Re(z * zeta^-k) = Re(z) cos(theta) + Im(z) sin(theta), theta = pi t / N
         acc = zr @ cos_t[t]
         if zi is not None:
             acc += zi @ sin_t[t]
-        out[:, k0:k0 + len(k)] = acc * (2.0 / n)
-    return out.reshape(z.shape[:-1] + (n,))
+        out[:, c0:c0 + len(k)] = acc * (2.0 / n)
+    return out.reshape(z.shape[:-1] + (len(kall),))
 
 
 def round_coeffs(m, delta: float) -> np.ndarray:

@@ -294,8 +294,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   const size_t o_bar = blob.add(bar.data(), L * 4);
   const size_t o_p256 = blob.add(p256.data(), p256.size() * 4);
   size_t o_perm = 0, o_fft = 0, o_rfft = 0, o_dct = 0;
-  const bool enc = log_n <= 15;
-  if (enc) {
+  {  // encode tables (every supported N)
     const uint32_t M = n / 2, P = n / 4;
     std::vector<uint32_t> perm(M);
     uint64_t e = 1;
@@ -369,7 +368,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   t.q_recip = reinterpret_cast<const double*>(base + o_qrec);
   t.barrett = reinterpret_cast<const uint32_t*>(base + o_bar);
   t.pow256 = reinterpret_cast<const uint32_t*>(base + o_p256);
-  if (enc) {
+  {
     t.slot_perm = reinterpret_cast<const uint32_t*>(base + o_perm);
     t.fft_tw = reinterpret_cast<const double2*>(base + o_fft);
     t.rfft_tw = reinterpret_cast<const double2*>(base + o_rfft);
@@ -464,13 +463,15 @@ int ckks_linear_encode_poly(const ckks_ctx* ctx, const double* slots, uint32_t c
                             double scale, uint32_t* pt, void* stream) {
   if (int rc = check_ctx(ctx)) return rc;
   if (int rc = check_limbs(ctx, limbs, 1)) return rc;
-  if (ctx->log_n > 15) return fail(CKKS_E_UNSUPPORTED, "full-polynomial encode needs log_n <= 15");
   if (!(scale > 0.0) || !std::isfinite(scale)) return fail(CKKS_E_INVALID_ARG, "scale must be finite and > 0");
   if (count == 0) return ok();
   if (int rc = check_ptr(slots, "slots")) return rc;
   if (int rc = check_ptr(pt, "pt")) return rc;
   if (overlaps(pt, size_t(count) * limbs * ctx->n * 4, slots, size_t(count) * (ctx->n / 2) * 8))
     return fail(CKKS_E_INVALID_ARG, "pt overlaps slots");
+  // at N = 2^16 the rows go through the batched transform (64 workgroups per row)
+  if (ctx->log_n == 16 && size_t(count) * limbs > 0x7FFFFFFFull / 64)
+    return fail(CKKS_E_INVALID_ARG, "count x limbs = %zu rows too many", size_t(count) * limbs);
   DeviceGuard guard(ctx->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = ckks::launch_encode_poly(ctx->t, slots, count, limbs, scale, pt, s);

@@ -121,7 +121,7 @@ hipError_t launch_ntt(const Tables& t, uint32_t* rows, size_t count_rows, uint32
 hipError_t launch_encode_scalar(const Tables& t, const double* w, size_t count, uint32_t limbs,
                                 double scale, uint32_t* w_enc, hipStream_t s);
 
-// NTT-form residues pt[count][limbs][N] of the encoded slot vectors (log_n <= 15).
+// NTT-form residues pt[count][limbs][N] of the encoded slot vectors.
 hipError_t launch_encode_poly(const Tables& t, const double* slots, uint32_t count, uint32_t limbs,
                               double scale, uint32_t* pt, hipStream_t s);
 

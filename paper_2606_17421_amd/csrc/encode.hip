@@ -47,7 +47,9 @@ __device__ __forceinline__ int spec_pad(int i) { return i + (i >> 5); }
 // other; the stage s+r butterfly on (x, x + d), d = P >> (s+r+1), multiplies
 // the difference by tw[(x mod d) << (s+r)].  Same results, in the same
 // positions, as R single stages; one LDS round trip and one barrier.
-template <int LOGP, int R>
+// TWS: the table holds the twiddles of a 2^(LOGP + TWS)-point transform
+// (exp(-2 pi i m / 2^(LOGP + TWS))), so this transform's are every 2^TWS-th.
+template <int LOGP, int R, int TWS = 0>
 __device__ __forceinline__ void fft_pass(double2* a, int s, const double2* __restrict__ tw, int nthreads) {
   constexpr int P = 1 << LOGP, G = 1 << R;
   const int span_lo = P >> (s + R);           // stride between a group's elements
@@ -66,7 +68,7 @@ __device__ __forceinline__ void fft_pass(double2* a, int s, const double2* __res
         const int i = x0 + (j & (h - 1)) * span_lo;   // index within the stage's half-block
         const double2 U = v[j], V = v[j + h];
         v[j] = cadd(U, V);
-        v[j + h] = cmul(csub(U, V), tw[i << (s + r)]);
+        v[j + h] = cmul(csub(U, V), tw[i << (s + r + TWS)]);
       }
     }
 #pragma unroll
@@ -256,6 +258,94 @@ __global__ __launch_bounds__(FusedPlan<LOGN>::T, WholePlan<LOGN>::kWavesPerSimd)
   }
 }
 
+// N = 2^16: the P = 2^14-point spectral transform (256 KiB of complex fp64)
+// does not fit the LDS.  Its first radix-2 decimation-in-frequency stage is
+// split off: A[n] = v[n] + v[n + P/2] and B[n] = (v[n] - v[n + P/2]) w_P^n,
+// whose P/2-point DFTs are the even and the odd outputs, X[2m] and X[2m + 1];
+// output k and its partner P - k have the same parity, so each half folds on
+// its own.  The halves go through the LDS in turn, each formed from the slot
+// vector gathered straight from global memory (it is as large as the LDS, and
+// the second gather costs less than holding B in registers), and each half's
+// coefficient residues are written for every limb before the next starts.
+// The limbs are taken to NTT form afterwards by the batched 2^16 transform.
+constexpr int kE16Threads = 1024;
+
+__global__ __launch_bounds__(kE16Threads) void encode_poly16_coeff_kernel(
+    Tables tb, const double* __restrict__ slots, uint32_t limbs, double scale, uint32_t* __restrict__ pt) {
+  constexpr int N = 1 << 16, M = N / 2, P = N / 4, H = P / 2, LOGH = 13, T = kE16Threads, KH = H / T;
+  __shared__ __align__(16) double2 a[H + (H >> 5)];  // spec_pad layout
+  const size_t b = blockIdx.x;
+  const double* z = slots + b * M;
+  uint32_t* out = pt + b * static_cast<size_t>(limbs) * N;
+  const int t = static_cast<int>(threadIdx.x);
+  // Makhoul order: v[n] = (y_2n, y_2n+1), y_u = z at the slot whose exponent is 2u+1 up to sign
+  auto y = [&](int m) {
+    const int u = m < M / 2 ? 2 * m : 2 * (M - 1 - m) + 1;
+    return z[tb.slot_perm[u]];
+  };
+  const double two_over_n = 2.0 / N;
+  auto brev = [](int x) { return static_cast<int>(__brev(static_cast<uint32_t>(x)) >> (32 - LOGH)); };
+#pragma unroll 1
+  for (int odd = 0; odd < 2; ++odd) {
+    if (odd) __syncthreads();  // every thread is done reading the even half
+#pragma unroll 2
+    for (int i = 0; i < KH; ++i) {
+      const int n = t + T * i;
+      const double2 v0 = make_double2(y(2 * n), y(2 * n + 1));
+      const double2 v1 = make_double2(y(2 * n + P), y(2 * n + P + 1));  // v[n + P/2]
+      a[spec_pad(n)] = odd ? cmul(csub(v0, v1), tb.fft_tw[n]) : cadd(v0, v1);
+    }
+    __syncthreads();
+    int s = 0;
+    for (; s + 3 <= LOGH; s += 3) fft_pass<LOGH, 3, 1>(a, s, tb.fft_tw, T);
+    fft_pass<LOGH, 1, 1>(a, s, tb.fft_tw, T);  // LOGH = 13: stages 0..11 by threes, then 12
+    // output k = 2m + odd at position brev(m); its partner P - k is output
+    // (H - m) mod H of the even half, H - 1 - m of the odd one.  Outputs go in
+    // batches of kB per thread (fewer live registers), each batch's residues
+    // written for every limb through buffer stores (a 32-bit lane offset per
+    // position; the limb's row as the scalar offset: a plaintext is at most 16
+    // limbs x 256 KiB).
+    const __amdgpu_buffer_rsrc_t ro =
+        __builtin_amdgcn_make_buffer_rsrc(out, 0, limbs * static_cast<uint32_t>(N) * 4u, 0x00020000);
+    constexpr int kB = 4;
+#pragma unroll 1
+    for (int i0 = 0; i0 < KH; i0 += kB) {
+      double p_lo[kB], p_hi[kB];
+#pragma unroll
+      for (int ii = 0; ii < kB; ++ii) {
+        const int m = t + T * (i0 + ii), k = 2 * m + odd;
+        const int mp = odd ? H - 1 - m : (H - m) & (H - 1);
+        const double2 ck = a[spec_pad(brev(m))], cm = a[spec_pad(brev(mp))];
+        const double2 cmc = make_double2(cm.x, -cm.y);
+        const double2 e = make_double2(0.5 * (ck.x + cmc.x), 0.5 * (ck.y + cmc.y));
+        const double2 dd = csub(ck, cmc);
+        const double2 o = make_double2(0.5 * dd.y, -0.5 * dd.x);
+        const double2 wo = cmul(tb.rfft_tw[k], o);
+        const double2 v_lo = cadd(e, wo), v_hi = csub(e, wo);
+        const double2 t_lo = tb.dct_tw[k], t_hi = tb.dct_tw[k + P];
+        p_lo[ii] = rint(scale * (two_over_n * (t_lo.x * v_lo.x - t_lo.y * v_lo.y)));
+        p_hi[ii] = rint(scale * (two_over_n * (t_hi.x * v_hi.x - t_hi.y * v_hi.y)));
+      }
+      // m_{N-k} = -m_k (0 < k < N/2), m_{N/2} = 0: index k and k + P from the
+      // outputs, N - k (N/2 for k = 0) and N - k - P their negations
+      for (uint32_t l = 0; l < limbs; ++l) {
+        const uint32_t q = tb.q[l];
+        const double qr = tb.q_recip[l];
+        const uint32_t so = l * static_cast<uint32_t>(N) * 4u;
+#pragma unroll
+        for (int ii = 0; ii < kB; ++ii) {
+          const uint32_t k = 2u * static_cast<uint32_t>(t + T * (i0 + ii)) + odd;
+          const uint32_t r = reduce_f64_int(p_lo[ii], q, qr), h = reduce_f64_int(p_hi[ii], q, qr);
+          __builtin_amdgcn_raw_buffer_store_b32(r, ro, k * 4u, so, 0);
+          __builtin_amdgcn_raw_buffer_store_b32(h, ro, (k + P) * 4u, so, 0);
+          __builtin_amdgcn_raw_buffer_store_b32(k ? (r ? q - r : 0u) : 0u, ro, (k ? N - k : M) * 4u, so, 0);
+          __builtin_amdgcn_raw_buffer_store_b32(h ? q - h : 0u, ro, (N - k - P) * 4u, so, 0);
+        }
+      }
+    }
+  }
+}
+
 template <int LOGN>
 hipError_t launch_poly(const Tables& t, const double* slots, uint32_t count, uint32_t limbs,
                        double scale, uint32_t* pt, hipStream_t s) {
@@ -284,6 +374,12 @@ hipError_t launch_encode_poly(const Tables& t, const double* slots, uint32_t cou
     case 13: return launch_poly<13>(t, slots, count, limbs, scale, pt, s);
     case 14: return launch_poly<14>(t, slots, count, limbs, scale, pt, s);
     case 15: return launch_poly<15>(t, slots, count, limbs, scale, pt, s);
+    case 16: {
+      encode_poly16_coeff_kernel<<<count, kE16Threads, 0, s>>>(t, slots, limbs, scale, pt);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      return launch_ntt(t, pt, static_cast<size_t>(count) * limbs, limbs, false, s);
+    }
     default: return hipErrorNotSupported;
   }
 }

@@ -263,6 +263,45 @@ def test_encode_poly_within_tolerance(gpu_lib, log_n, limbs, count):
     assert mismatches <= max(2, count * n // 100000)
 
 
+@pytest.mark.parametrize("log_scale", [30, 40])
+def test_encode_poly_n16_sampled_coefficients(gpu_lib, log_scale):
+    """N = 2^16 (split spectral transform, then the batched 2^16 NTT): constant
+    slots give the constant polynomial exactly in every NTT slot; for random
+    slots every limb's plaintext, taken back to coefficients by the oracle's
+    inverse transform, equals the oracle's rounded coefficients at 1024 sampled
+    indices (k = 0, 1, N/2 - 1, N/2, N/2 + 1, N - 1 and random ones, both
+    parities and all four quarters), except at fp64 rounding ties."""
+    ck = gpu_lib
+    log_n, limbs, count = 16, 3, 2
+    ctx = ctx_for(ck, log_n, limbs)
+    qs, psis, n = ctx.moduli, ctx.roots, 1 << log_n
+    delta = 2.0 ** log_scale
+    z = gen.poly_weights(np.random.default_rng(160 + log_scale), 1, count, n // 2)[0]
+    if log_scale == 40:
+        z = z + 4.0                                           # coefficients near 2^42
+    z[0, :] = 0.25
+    pt = ck.empty_u32((count, limbs, n))
+    ck.ckks_linear_encode_poly(ctx, ck.to_device(z), count, limbs, delta, pt)
+    got = ck.to_host_u32(pt)
+    c0 = round(0.25 * delta)
+    for l in range(limbs):
+        assert np.all(got[0, l] == np.uint32(c0 % qs[l])), l
+    rng = np.random.default_rng(7)
+    ks = np.unique(np.concatenate([[0, 1, n // 2 - 1, n // 2, n // 2 + 1, n - 1],
+                                   rng.choice(n, 1018, replace=False)]))
+    want = OE.round_coeffs(OE.encode_coeffs(z[1], log_n, ks), delta)
+    bad = 0
+    for l in range(limbs):
+        coef = ON.intt(got[1, l].astype(np.uint64), qs[l], psis[l], log_n).astype(np.int64)
+        w = np.mod(want, qs[l])
+        diff = np.mod(coef[ks] - w, qs[l])
+        off = diff != 0
+        assert np.all((diff[off] == 1) | (diff[off] == qs[l] - 1)), (l, diff[off][:8])
+        bad += int(np.sum(off))
+    print(f"encode_poly N=2^16 scale 2^{log_scale}: {bad} of {limbs * len(ks)} sampled residues off by one")
+    assert bad <= 2
+
+
 @pytest.mark.parametrize("log_n,limbs", [(10, 3), (14, 3), (15, 2)])
 def test_encode_poly_large_coefficients(gpu_lib, log_n, limbs):
     """Slots offset by 4.0 at scale 2^30: coefficients beyond 2^31 take the

@@ -118,3 +118,13 @@ def test_slot_order_is_powers_of_five():
     for j in (0, 1, 2, 3, 7, n // 2 - 1):
         point = np.exp(1j * np.pi * pow(5, j, 2 * n) / n)
         assert abs(np.polyval(m[::-1], point) - z[j]) < 1e-11
+
+
+def test_selected_coefficients_match_the_full_sum():
+    """encode_coeffs(z, log_n, ks) gives column ks of the full inverse embedding
+    (the full form is pinned above), including k = 0, N/2 and N - 1."""
+    log_n = 8
+    n = 1 << log_n
+    z = np.random.default_rng(5).normal(0, 0.02, (2, n // 2))
+    ks = np.array([0, 1, 7, n // 4, n // 2, n // 2 + 3, n - 1])
+    assert np.array_equal(E.encode_coeffs(z, log_n, ks), E.encode_coeffs(z, log_n)[:, ks])
