@@ -13,10 +13,10 @@
 //
 // Encryption and decryption run the batched NTT kernels over the c0 rows (or
 // the output rows) through their row-group stride, with pointwise passes
-// around them, 16 bytes per thread and limb.  The refresh, up to N = 2^14, is
+// around them, 16 bytes per thread and limb.  The refresh, up to N = 2^15, is
 // two transform kernels (decrypt + inverse, lift + forward + combine), or up to
-// 2^13 for decode-size counts one fused kernel split by output limb; above
-// 2^14 it is the pass structure of encryption and decryption.
+// 2^13 for decode-size counts one fused kernel split by output limb; at 2^16
+// (a row exceeds the LDS) it is the pass structure of encryption and decryption.
 #include "ntt_core.hpp"
 
 namespace ckks {
@@ -299,9 +299,9 @@ __global__ __launch_bounds__(RefreshPlan<LOGN>::P::T, RefreshPlan<LOGN>::kWavesP
   }
 }
 
-// Two-kernel refresh for N <= 2^14: the same arithmetic as the fused kernel,
+// Two-kernel refresh for N <= 2^15: the same arithmetic as the fused kernel,
 // with each transform in a workgroup of its own and the whole-row plan's
-// occupancy (two workgroups per CU).
+// occupancy (two workgroups per CU up to 2^14, one at 2^15).
 // (1) per (ciphertext, limb 0 or 1): c0 + c1 (.) s read coalesced, inverse
 //     transform, the coefficient residues written to c1 row 0 / 1 of ct_out
 //     (scratch);
@@ -493,7 +493,9 @@ hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs
   // three transforms (64 ciphertexts x 4 limbs at 2^13: 26.7 against 30.7 us);
   // larger ones, and every count at 2^14 (its fused workgroup is 1024
   // threads), the two-kernel route (32 ciphertexts at 2^14: 40.9 against
-  // 41.8 us; 128: 62.5 against 89.5 us; 768: 0.36 against 0.52 ms).
+  // 41.8 us; 128: 62.5 against 89.5 us; 768: 0.36 against 0.52 ms).  At 2^15
+  // it replaces the pointwise passes (768 ciphertexts x 4 limbs: 0.79 against
+  // 1.01 ms; 32: 66 against 72 us).
   if (t.log_n >= 14 || static_cast<size_t>(count) * limbs_out > t.num_cus) {
     switch (t.log_n) {
       case 10: return launch_refresh_two<10>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
@@ -501,6 +503,7 @@ hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs
       case 12: return launch_refresh_two<12>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
       case 13: return launch_refresh_two<13>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
       case 14: return launch_refresh_two<14>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
+      case 15: return launch_refresh_two<15>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
       default: break;
     }
   }
@@ -511,8 +514,8 @@ hipError_t launch_refresh(const Tables& t, const uint32_t* ct_in, uint32_t limbs
     case 13: return launch_refresh_fused<13>(t, ct_in, limbs_in, s_ntt, a, e, count, limbs_out, ct_out, s);
     default: break;
   }
-  // N >= 2^15: pointwise passes around the batched transforms (at 2^15 the
-  // fused kernel's 32 residues per thread would spill)
+  // N = 2^16 (a row exceeds the LDS): pointwise passes around the batched
+  // transforms
   const uint32_t grid = quad_grid(t.n, count);
   const uint32_t gs = 2 * limbs_out;
   // 1. limbs 0 and 1 of c0 + c1 (.) s into the c1 rows 0, 1 of ct_out (scratch), then INTT them

@@ -79,11 +79,11 @@ def test_decrypt_bit_exact(gpu_lib, log_n, limbs, count):
 
 
 # Routes on 256 CUs: fused for N <= 2^13 with at most 256 (ciphertext, output limb) pairs
-# (64 x 4 at 2^13 is the largest), the two-kernel route otherwise (every 2^14 case),
-# pointwise passes at 2^16.
+# (64 x 4 at 2^13 is the largest), the two-kernel route otherwise (every 2^14 and
+# 2^15 case), pointwise passes at 2^16.
 @pytest.mark.parametrize("log_n,L,limbs_in,limbs_out,count", [(10, 4, 2, 4, 4), (14, 4, 3, 4, 3), (12, 5, 4, 2, 2),
                                                               (16, 3, 2, 3, 2), (10, 3, 2, 3, 160), (13, 4, 3, 4, 200),
-                                                              (13, 4, 3, 4, 64)])
+                                                              (13, 4, 3, 4, 64), (15, 5, 3, 5, 3)])
 def test_refresh_bit_exact(gpu_lib, log_n, L, limbs_in, limbs_out, count):
     ck = gpu_lib
     ctx, qs, psis, n, st, s, s_ntt, m, e, a = setup(ck, log_n, L, count, 340 + log_n)
