@@ -182,8 +182,9 @@ __device__ __forceinline__ void wave_relayout(uint32_t (&v)[1 << LOGE], uint32_t
 }
 
 // Forward transform of one block held in registers in group-0 layout; on
-// return the registers hold group NG-1 layout.
-template <int LOGN, int LOGB, int LOGE, int G = 0>
+// return the registers hold group NG-1 layout, in [0, q) (kNorm) or left in
+// the lazy range [0, 4q) for a consumer that reduces anyway.
+template <int LOGN, int LOGB, int LOGE, int G = 0, bool kNorm = true>
 __device__ __forceinline__ void fwd_block(uint32_t (&v)[1 << LOGE], uint32_t t, uint32_t blk,
                                           const uint32_t* __restrict__ tw,
                                           const uint32_t* __restrict__ tws, uint32_t q,
@@ -192,14 +193,25 @@ __device__ __forceinline__ void fwd_block(uint32_t (&v)[1 << LOGE], uint32_t t, 
   if constexpr (G > 0) exchange<LOGB, LOGE, G - 1, G>(v, t, lds);
   fwd_group<LOGN, LOGB, LOGE, G>(v, t, blk, tw, tws, q);
   if constexpr (G + 1 < P::NG) {
-    fwd_block<LOGN, LOGB, LOGE, G + 1>(v, t, blk, tw, tws, q, lds);
-  } else {
+    fwd_block<LOGN, LOGB, LOGE, G + 1, kNorm>(v, t, blk, tw, tws, q, lds);
+  } else if constexpr (kNorm) {
 #pragma unroll
     for (int j = 0; j < P::E; ++j) {  // [0, 4q) -> [0, q)
       uint32_t x = min(v[j], v[j] - 2 * q);
       v[j] = min(x, x - q);
     }
   }
+}
+
+// (c - v) w mod q in [0, q) for c in [0, q) and a lazy forward output v in
+// [0, 4q), w < q with its Shoup companion ws: v mod 2q, then c + 2q - v in
+// (0, 3q) < 2^32 through the lazy Shoup product and one conditional
+// subtraction (10 operations against 14 with v normalised first).
+__device__ __forceinline__ uint32_t sub_lazy_mul_shoup(uint32_t c, uint32_t v, uint32_t w, uint32_t ws,
+                                                       uint32_t q) {
+  const uint32_t r = min(v, v - 2 * q);
+  const uint32_t y = mul_shoup_lazy(c + 2 * q - r, w, ws, q);
+  return min(y, y - q);
 }
 
 // Inverse transform (without the N^-1 factor) of one block held in group

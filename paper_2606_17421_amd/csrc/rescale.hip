@@ -64,19 +64,19 @@ __global__ __launch_bounds__((WholePlan<LOGN, kSplit>::P::T), (WholePlan<LOGN, k
 #pragma unroll
     for (int j = 0; j < P::E; ++j) v[j] = static_cast<uint32_t>(r[j] < 0 ? r[j] + static_cast<int32_t>(q) : r[j]);
     const size_t tl = static_cast<size_t>(l) << LOGN;
-    fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+    fwd_block<LOGN, LOGN, LOGE, 0, false>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);  // [0, 4q)
     const uint32_t qi = tb.qinv[top * tb.L + l], qis = tb.qinv_shoup[top * tb.L + l];
     if constexpr (kCoalesce) {
       wave_relayout<LOGN, LOGE, false>(v, t, lds);
       const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
       uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-      for (int j = 0; j < P::E; ++j) dl[j << 6] = mul_shoup(sub_mod(sl[j << 6], v[j], q), qi, qis, q);
+      for (int j = 0; j < P::E; ++j) dl[j << 6] = sub_lazy_mul_shoup(sl[j << 6], v[j], qi, qis, q);
     } else {
 #pragma unroll
       for (int j = 0; j < P::E; ++j) {
         const size_t x = static_cast<size_t>(l) * N + P::template pos<P::NG - 1>(t, j);
-        dst[x] = mul_shoup(sub_mod(src[x], v[j], q), qi, qis, q);
+        dst[x] = sub_lazy_mul_shoup(src[x], v[j], qi, qis, q);
       }
     }
   }
@@ -176,18 +176,18 @@ rescale2_fwd_kernel(Tables tb, const uint32_t* __restrict__ in, const uint32_t* 
 #pragma unroll
   for (int j = 0; j < P::E; ++j) v[j] = add_mod(mul_shoup(lift(r1[j], q), ti, tis, q), lift(r2[j], q), q);
   const size_t tl = static_cast<size_t>(l) << LOGN;
-  fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+  fwd_block<LOGN, LOGN, LOGE, 0, false>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);  // [0, 4q)
   if constexpr (kCoalesce) {
     wave_relayout<LOGN, LOGE, false>(v, t, lds);
     const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
     uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) dl[j << 6] = mul_shoup(sub_mod(mul_shoup(sl[j << 6], ti, tis, q), v[j], q), ui, uis, q);
+    for (int j = 0; j < P::E; ++j) dl[j << 6] = sub_lazy_mul_shoup(mul_shoup(sl[j << 6], ti, tis, q), v[j], ui, uis, q);
   } else {
 #pragma unroll
     for (int j = 0; j < P::E; ++j) {
       const size_t x = static_cast<size_t>(l) * N + P::template pos<P::NG - 1>(t, j);
-      dst[x] = mul_shoup(sub_mod(mul_shoup(src[x], ti, tis, q), v[j], q), ui, uis, q);
+      dst[x] = sub_lazy_mul_shoup(mul_shoup(src[x], ti, tis, q), v[j], ui, uis, q);
     }
   }
 }
@@ -290,7 +290,7 @@ __global__ __launch_bounds__(kBlkThreads) void rescale16_blocks_combine_kernel(
 #pragma unroll
   for (int j = 0; j < P::E; ++j) v[j] = b[P::template pos<0>(t, j)];
   const size_t tl = static_cast<size_t>(l) << 16;
-  fwd_block<16, kBlkLogB, kBlkLogE>(v, t, blk, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+  fwd_block<16, kBlkLogB, kBlkLogE, 0, false>(v, t, blk, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);  // [0, 4q)
   const uint32_t qi = tb.qinv[top * tb.L + l], qis = tb.qinv_shoup[top * tb.L + l];
   const uint32_t* c = in + ((p0 + r) * limbs + l) * 65536 + boff;
   uint32_t* o = out + ((p0 + r) * (limbs - 1) + l) * 65536 + boff;
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(kBlkThreads) void rescale16_blocks_combine_kernel(
 #pragma unroll
   for (int j = 0; j < P::E; ++j) {
     const uint32_t x = t + 64 * j;  // coalesced
-    o[x] = mul_shoup(sub_mod(c[x], v[j], q), qi, qis, q);
+    o[x] = sub_lazy_mul_shoup(c[x], v[j], qi, qis, q);
   }
 }
 
