@@ -433,7 +433,7 @@ moddown_combine_kernel(Tables tb, const uint32_t* __restrict__ acc, const uint32
 #pragma unroll
     for (int j = 0; j < P::E; ++j) v[j] = static_cast<uint32_t>(r[j] < 0 ? r[j] + static_cast<int32_t>(q) : r[j]);
     const size_t tl = static_cast<size_t>(l) << LOGN;
-    fwd_block<LOGN, LOGN, LOGE>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);
+    fwd_block<LOGN, LOGN, LOGE, 0, false>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);  // [0, 4q)
     wave_relayout<LOGN, LOGE, false>(v, t, lds);
     const uint32_t pi = tb.qinv[top * tb.L + l], pis = tb.qinv_shoup[top * tb.L + l];
     const uint32_t* sl = src + static_cast<size_t>(l) * N;
@@ -442,12 +442,12 @@ moddown_combine_kernel(Tables tb, const uint32_t* __restrict__ acc, const uint32
       const uint32_t* c0l = c0 + static_cast<size_t>(l) * N;
 #pragma unroll
       for (int j = 0; j < P::E; ++j) {
-        const uint32_t u = mul_shoup(sub_mod(sl[j << 6], v[j], q), pi, pis, q);
+        const uint32_t u = sub_lazy_mul_shoup(sl[j << 6], v[j], pi, pis, q);
         dl[j << 6] = add_mod(u, c0l[perm_src(c_base + (j << 6), x.g, LOGN)], q);
       }
     } else {
 #pragma unroll
-      for (int j = 0; j < P::E; ++j) dl[j << 6] = mul_shoup(sub_mod(sl[j << 6], v[j], q), pi, pis, q);
+      for (int j = 0; j < P::E; ++j) dl[j << 6] = sub_lazy_mul_shoup(sl[j << 6], v[j], pi, pis, q);
     }
   }
 }
