@@ -293,16 +293,18 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   const size_t o_qrec = blob.add(qrec.data(), L * 8);
   const size_t o_bar = blob.add(bar.data(), L * 4);
   const size_t o_p256 = blob.add(p256.data(), p256.size() * 4);
-  size_t o_perm = 0, o_fft = 0, o_rfft = 0, o_dct = 0;
+  size_t o_perm = 0, o_pos = 0, o_fft = 0, o_rfft = 0, o_dct = 0;
   {  // encode tables (every supported N)
     const uint32_t M = n / 2, P = n / 4;
-    std::vector<uint32_t> perm(M);
+    std::vector<uint32_t> perm(M), pos(M);
     uint64_t e = 1;
     for (uint32_t j = 0; j < M; ++j) {
       const uint64_t t = e < n ? e : two_n - e;  // odd, < N
       perm[(t - 1) / 2] = j;
       e = e * 5 % two_n;
     }
+    // Makhoul order: y_m = z at perm[u], u = 2m (m < M/2) or 2(M - 1 - m) + 1
+    for (uint32_t u = 0; u < M; ++u) pos[perm[u]] = (u % 2 == 0) ? u / 2 : M - 1 - (u - 1) / 2;
     const long double pi = 3.141592653589793238462643383279502884L;
     std::vector<double2> fft(P / 2), rfft(P), dct(M);
     for (uint32_t m = 0; m < P / 2; ++m) {
@@ -318,6 +320,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
       dct[k] = make_double2(static_cast<double>(cosl(a)), static_cast<double>(sinl(a)));
     }
     o_perm = blob.add(perm.data(), perm.size() * 4);
+    o_pos = blob.add(pos.data(), pos.size() * 4);
     o_fft = blob.add(fft.data(), fft.size() * sizeof(double2));
     o_rfft = blob.add(rfft.data(), rfft.size() * sizeof(double2));
     o_dct = blob.add(dct.data(), dct.size() * sizeof(double2));
@@ -370,6 +373,7 @@ int ckks_ctx_create(ckks_ctx** out, uint32_t log_n, uint32_t num_limbs, const ui
   t.pow256 = reinterpret_cast<const uint32_t*>(base + o_p256);
   {
     t.slot_perm = reinterpret_cast<const uint32_t*>(base + o_perm);
+    t.slot_pos = reinterpret_cast<const uint32_t*>(base + o_pos);
     t.fft_tw = reinterpret_cast<const double2*>(base + o_fft);
     t.rfft_tw = reinterpret_cast<const double2*>(base + o_rfft);
     t.dct_tw = reinterpret_cast<const double2*>(base + o_dct);

@@ -35,8 +35,9 @@ struct Tables {
   const double* q_recip;       // [L]     1.0 / q_l rounded to nearest
   const uint32_t* barrett;     // [L]     floor(2^61 / q_l) (< 2^32 for q_l > 2^29)
   const uint32_t* pow256;      // [L][8]  256^s mod q_l, s < 8
-  // Encode tables (present when log_n <= 15; M = N/2, P = N/4).
+  // Encode tables (M = N/2, P = N/4).
   const uint32_t* slot_perm;   // [M]  slot index j whose odd exponent is 2u+1 (up to sign)
+  const uint32_t* slot_pos;    // [M]  index m of slot j in the Makhoul-ordered real sequence
   const double2* fft_tw;       // [P/2] exp(-2 pi i m / P)
   const double2* rfft_tw;      // [P]   exp(-2 pi i k / M)
   const double2* dct_tw;       // [M]   exp(-i pi k / (2M))

@@ -263,12 +263,16 @@ __global__ __launch_bounds__(FusedPlan<LOGN>::T, WholePlan<LOGN>::kWavesPerSimd)
 // split off: A[n] = v[n] + v[n + P/2] and B[n] = (v[n] - v[n + P/2]) w_P^n,
 // whose P/2-point DFTs are the even and the odd outputs, X[2m] and X[2m + 1];
 // output k and its partner P - k have the same parity, so each half folds on
-// its own.  The halves go through the LDS in turn, each formed from the slot
-// vector gathered straight from global memory (it is as large as the LDS, and
-// the second gather costs less than holding B in registers), and each half's
-// coefficient residues are written for every limb before the next starts.
-// The limbs are taken to NTT form afterwards by the batched 2^16 transform.
+// its own.  The plaintext's own first 256 KiB serve as scratch: the slot
+// vector is read coalesced and scattered into Makhoul order there (v), A and
+// B are read back coalesced (A into the LDS, B into registers), and the even
+// half's rounded coefficients wait there while the odd half is transformed.
+// Each thread then holds outputs 2m and 2m + 1 and writes every limb's
+// residues as 8-byte pairs, whole cache lines per wave (the halves written
+// apart would leave every line half-written twice).  The limbs are taken to
+// NTT form afterwards by the batched 2^16 transform.
 constexpr int kE16Threads = 1024;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __global__ __launch_bounds__(kE16Threads) void encode_poly16_coeff_kernel(
     Tables tb, const double* __restrict__ slots, uint32_t limbs, double scale, uint32_t* __restrict__ pt) {
@@ -278,69 +282,98 @@ __global__ __launch_bounds__(kE16Threads) void encode_poly16_coeff_kernel(
   const double* z = slots + b * M;
   uint32_t* out = pt + b * static_cast<size_t>(limbs) * N;
   const int t = static_cast<int>(threadIdx.x);
-  // Makhoul order: v[n] = (y_2n, y_2n+1), y_u = z at the slot whose exponent is 2u+1 up to sign
-  auto y = [&](int m) {
-    const int u = m < M / 2 ? 2 * m : 2 * (M - 1 - m) + 1;
-    return z[tb.slot_perm[u]];
-  };
+  // v[n] = (y_2n, y_2n+1) as doubles y_m at vs[m]: slot j lands at its Makhoul index
+  double* vs = reinterpret_cast<double*>(out);
+#pragma unroll 4
+  for (int i = 0; i < M / T; ++i) {
+    const int j = t + T * i;
+    vs[tb.slot_pos[j]] = z[j];
+  }
+  __syncthreads();  // the scattered sequence is visible to the whole workgroup
+  const double2* v2 = reinterpret_cast<const double2*>(vs);
+  double2 bv[KH];
+#pragma unroll
+  for (int i = 0; i < KH; ++i) {
+    const int n = t + T * i;
+    const double2 v0 = v2[n], v1 = v2[n + H];
+    a[spec_pad(n)] = cadd(v0, v1);
+    bv[i] = cmul(csub(v0, v1), tb.fft_tw[n]);
+  }
   const double two_over_n = 2.0 / N;
   auto brev = [](int x) { return static_cast<int>(__brev(static_cast<uint32_t>(x)) >> (32 - LOGH)); };
-#pragma unroll 1
-  for (int odd = 0; odd < 2; ++odd) {
-    if (odd) __syncthreads();  // every thread is done reading the even half
-#pragma unroll 2
-    for (int i = 0; i < KH; ++i) {
-      const int n = t + T * i;
-      const double2 v0 = make_double2(y(2 * n), y(2 * n + 1));
-      const double2 v1 = make_double2(y(2 * n + P), y(2 * n + P + 1));  // v[n + P/2]
-      a[spec_pad(n)] = odd ? cmul(csub(v0, v1), tb.fft_tw[n]) : cadd(v0, v1);
-    }
+  // Rounded coefficients k and k + P of output k = 2m + odd, which sits at
+  // position brev(m); its partner P - k is output (H - m) mod H of the even
+  // half, H - 1 - m of the odd one.
+  auto fold = [&](int m, int odd, double& p_lo, double& p_hi) {
+    const int k = 2 * m + odd;
+    const int mp = odd ? H - 1 - m : (H - m) & (H - 1);
+    const double2 ck = a[spec_pad(brev(m))], cm = a[spec_pad(brev(mp))];
+    const double2 cmc = make_double2(cm.x, -cm.y);
+    const double2 e = make_double2(0.5 * (ck.x + cmc.x), 0.5 * (ck.y + cmc.y));
+    const double2 dd = csub(ck, cmc);
+    const double2 o = make_double2(0.5 * dd.y, -0.5 * dd.x);
+    const double2 wo = cmul(tb.rfft_tw[k], o);
+    const double2 v_lo = cadd(e, wo), v_hi = csub(e, wo);
+    const double2 t_lo = tb.dct_tw[k], t_hi = tb.dct_tw[k + P];
+    p_lo = rint(scale * (two_over_n * (t_lo.x * v_lo.x - t_lo.y * v_lo.y)));
+    p_hi = rint(scale * (two_over_n * (t_hi.x * v_hi.x - t_hi.y * v_hi.y)));
+  };
+  auto half_fft = [&]() {
     __syncthreads();
     int s = 0;
     for (; s + 3 <= LOGH; s += 3) fft_pass<LOGH, 3, 1>(a, s, tb.fft_tw, T);
     fft_pass<LOGH, 1, 1>(a, s, tb.fft_tw, T);  // LOGH = 13: stages 0..11 by threes, then 12
-    // output k = 2m + odd at position brev(m); its partner P - k is output
-    // (H - m) mod H of the even half, H - 1 - m of the odd one.  Outputs go in
-    // batches of kB per thread (fewer live registers), each batch's residues
-    // written for every limb through buffer stores (a 32-bit lane offset per
-    // position; the limb's row as the scalar offset: a plaintext is at most 16
-    // limbs x 256 KiB).
-    const __amdgpu_buffer_rsrc_t ro =
-        __builtin_amdgcn_make_buffer_rsrc(out, 0, limbs * static_cast<uint32_t>(N) * 4u, 0x00020000);
-    constexpr int kB = 4;
+  };
+  // even half; its coefficients (k = 2m, 2m + P) wait at vs[m], vs[H + m]
+  // (every read of v is done: the transform's barriers come first)
+  half_fft();
+#pragma unroll
+  for (int i = 0; i < KH; ++i) {
+    __builtin_amdgcn_sched_barrier(0);
+    const int m = t + T * i;
+    double p_lo, p_hi;
+    fold(m, 0, p_lo, p_hi);
+    vs[m] = p_lo;
+    vs[H + m] = p_hi;
+  }
+  __syncthreads();  // every thread is done reading the even half
+#pragma unroll
+  for (int i = 0; i < KH; ++i) a[spec_pad(t + T * i)] = bv[i];
+  half_fft();
+  // odd half, then each pair (2m, 2m + 1) for every limb.  m_{N-k} = -m_k
+  // (0 < k < N/2), m_{N/2} = 0.  Limb 0's stores at 2m and 2m + P overwrite
+  // only this thread's own waiting values vs[m], vs[H + m], read just before;
+  // the mirrored positions lie above the scratch.  Buffer stores: a 32-bit
+  // lane offset per position, the limb's row as the scalar offset (a
+  // plaintext is at most 16 limbs x 256 KiB).
+  const __amdgpu_buffer_rsrc_t ro =
+      __builtin_amdgcn_make_buffer_rsrc(out, 0, limbs * static_cast<uint32_t>(N) * 4u, 0x00020000);
+  constexpr int kB = 2;
 #pragma unroll 1
-    for (int i0 = 0; i0 < KH; i0 += kB) {
-      double p_lo[kB], p_hi[kB];
+  for (int i0 = 0; i0 < KH; i0 += kB) {
+    double e_lo[kB], e_hi[kB], o_lo[kB], o_hi[kB];
+#pragma unroll
+    for (int ii = 0; ii < kB; ++ii) {
+      const int m = t + T * (i0 + ii);
+      fold(m, 1, o_lo[ii], o_hi[ii]);
+      e_lo[ii] = vs[m];
+      e_hi[ii] = vs[H + m];
+    }
+    for (uint32_t l = 0; l < limbs; ++l) {
+      const uint32_t q = tb.q[l];
+      const double qr = tb.q_recip[l];
+      const uint32_t so = l * static_cast<uint32_t>(N) * 4u;
 #pragma unroll
       for (int ii = 0; ii < kB; ++ii) {
-        const int m = t + T * (i0 + ii), k = 2 * m + odd;
-        const int mp = odd ? H - 1 - m : (H - m) & (H - 1);
-        const double2 ck = a[spec_pad(brev(m))], cm = a[spec_pad(brev(mp))];
-        const double2 cmc = make_double2(cm.x, -cm.y);
-        const double2 e = make_double2(0.5 * (ck.x + cmc.x), 0.5 * (ck.y + cmc.y));
-        const double2 dd = csub(ck, cmc);
-        const double2 o = make_double2(0.5 * dd.y, -0.5 * dd.x);
-        const double2 wo = cmul(tb.rfft_tw[k], o);
-        const double2 v_lo = cadd(e, wo), v_hi = csub(e, wo);
-        const double2 t_lo = tb.dct_tw[k], t_hi = tb.dct_tw[k + P];
-        p_lo[ii] = rint(scale * (two_over_n * (t_lo.x * v_lo.x - t_lo.y * v_lo.y)));
-        p_hi[ii] = rint(scale * (two_over_n * (t_hi.x * v_hi.x - t_hi.y * v_hi.y)));
-      }
-      // m_{N-k} = -m_k (0 < k < N/2), m_{N/2} = 0: index k and k + P from the
-      // outputs, N - k (N/2 for k = 0) and N - k - P their negations
-      for (uint32_t l = 0; l < limbs; ++l) {
-        const uint32_t q = tb.q[l];
-        const double qr = tb.q_recip[l];
-        const uint32_t so = l * static_cast<uint32_t>(N) * 4u;
-#pragma unroll
-        for (int ii = 0; ii < kB; ++ii) {
-          const uint32_t k = 2u * static_cast<uint32_t>(t + T * (i0 + ii)) + odd;
-          const uint32_t r = reduce_f64_int(p_lo[ii], q, qr), h = reduce_f64_int(p_hi[ii], q, qr);
-          __builtin_amdgcn_raw_buffer_store_b32(r, ro, k * 4u, so, 0);
-          __builtin_amdgcn_raw_buffer_store_b32(h, ro, (k + P) * 4u, so, 0);
-          __builtin_amdgcn_raw_buffer_store_b32(k ? (r ? q - r : 0u) : 0u, ro, (k ? N - k : M) * 4u, so, 0);
-          __builtin_amdgcn_raw_buffer_store_b32(h ? q - h : 0u, ro, (N - k - P) * 4u, so, 0);
-        }
+        const uint32_t m = static_cast<uint32_t>(t + T * (i0 + ii));
+        const uint32_t r0 = reduce_f64_int(e_lo[ii], q, qr), r1 = reduce_f64_int(o_lo[ii], q, qr);
+        const uint32_t h0 = reduce_f64_int(e_hi[ii], q, qr), h1 = reduce_f64_int(o_hi[ii], q, qr);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{r0, r1}, ro, 2u * m * 4u, so, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{h0, h1}, ro, (2u * m + P) * 4u, so, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(m ? (r0 ? q - r0 : 0u) : 0u, ro, (m ? N - 2u * m : M) * 4u, so, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(r1 ? q - r1 : 0u, ro, (N - 2u * m - 1u) * 4u, so, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(h0 ? q - h0 : 0u, ro, (N - 2u * m - P) * 4u, so, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(h1 ? q - h1 : 0u, ro, (N - 2u * m - 1u - P) * 4u, so, 0);
       }
     }
   }
