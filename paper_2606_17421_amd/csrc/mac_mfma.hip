@@ -94,11 +94,19 @@ __device__ __forceinline__ void to_fragments(const uint32_t (&x)[16], v4i (&f)[4
 // Weight digits: adig[((l * mt_total + mt) * ks_total + ks) * 4 + a][lane] holds
 // e_a(w[mt*16 + lane%16][ks*64 + (lane/16)*16 + i]) in byte i (zero-padded);
 // flags[l * mt_total + mt] != 0 when any e_3 of that 16-row tile is non-zero.
+// One workgroup per (tile, limb).  The limbs of a weight are adjacent in w_enc,
+// so the workgroups of one tile read the same cache lines: their logical ids
+// are consecutive and each XCD runs a contiguous range of them, so a tile's
+// rows come from HBM once into that XCD's L2 (with the limb as the slow grid
+// dimension every line was fetched about once per limb).
 __global__ __launch_bounds__(kThreads) void mfma_prep_kernel(
     const uint32_t* __restrict__ qtab, const uint32_t* __restrict__ w_enc, uint32_t d_out,
     uint32_t d_in, uint32_t limbs, uint32_t mt_total, uint32_t ks_total, v4i* __restrict__ adig,
     uint32_t* __restrict__ flags) {
-  const uint32_t mt = blockIdx.x, l = blockIdx.y;
+  const uint32_t G = gridDim.x;
+  uint32_t lid = blockIdx.x;
+  if ((G & 7u) == 0) lid = (lid & 7u) * (G >> 3) + (lid >> 3);
+  const uint32_t mt = lid / limbs, l = lid - mt * limbs;
   const uint32_t q = qtab[l];
   uint32_t top = 0;
   for (uint32_t idx = threadIdx.x; idx < ks_total * 64; idx += kThreads) {
@@ -512,8 +520,8 @@ hipError_t launch_mac_scalar_mfma(const Tables& t, const uint32_t* w_enc, const 
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   v4i* adig = reinterpret_cast<v4i*>(ws);
   uint32_t* flags = reinterpret_cast<uint32_t*>(ws + s.adig_bytes);
-  mfma_prep_kernel<<<dim3(s.mt_total, limbs), kThreads, 0, st>>>(t.q, w_enc, d_out, d_in, limbs, s.mt_total,
-                                                                 s.ks_total, adig, flags);
+  mfma_prep_kernel<<<dim3(s.mt_total * limbs), kThreads, 0, st>>>(t.q, w_enc, d_out, d_in, limbs, s.mt_total,
+                                                                  s.ks_total, adig, flags);
   const size_t grid = static_cast<size_t>(limbs) * s.tiles_n * s.tiles_m;
   if (grid >= (size_t(1) << 31)) return hipErrorInvalidValue;  // tile indices are 32-bit
   if (d_in <= kCsMaxDin) {
