@@ -35,18 +35,21 @@ __global__ __launch_bounds__((WholePlan<LOGN, kSplit>::P::T), (WholePlan<LOGN, k
   const uint32_t qt = tb.q[top];
 
   // Up to 2^14 the rows are read and written in the wave-coalesced layout
-  // (re-laid out through each wave's LDS region), non-temporally (each row is
-  // touched once); at 2^15 the extra live registers of that path cost more
-  // than the coalescing gains, and there a wave's load or store of one element
-  // index covers 64 different cache lines, which the following indices reuse:
-  // those accesses must stay cached (non-temporal: 3.7 -> 6.3 ms at 3072
-  // ciphertexts of 6 limbs).
+  // (re-laid out through each wave's LDS region), non-temporally when one
+  // workgroup takes a whole polynomial (each row is touched once).  The split
+  // route re-reads the top row in every limb's workgroup and keeps all its
+  // accesses cached (non-temporal there: 12.3 -> 13.3-13.8 us for 32
+  // ciphertexts at 2^13, 4 limbs).  At 2^15 the extra live registers of the
+  // coalesced path cost more than the coalescing gains, and there a wave's
+  // load or store of one element index covers 64 different cache lines, which
+  // the following indices reuse: those accesses must stay cached
+  // (non-temporal: 3.7 -> 6.3 ms at 3072 ciphertexts of 6 limbs).
   constexpr bool kCoalesce = LOGN <= 14;
   uint32_t v[P::E];
   if constexpr (kCoalesce) {
     const uint32_t* stop = src + static_cast<size_t>(top) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) v[j] = __builtin_nontemporal_load(&stop[j << 6]);
+    for (int j = 0; j < P::E; ++j) v[j] = kSplit ? stop[j << 6] : __builtin_nontemporal_load(&stop[j << 6]);
     wave_relayout<LOGN, LOGE, true>(v, t, lds);
   } else {
 #pragma unroll
@@ -75,9 +78,11 @@ __global__ __launch_bounds__((WholePlan<LOGN, kSplit>::P::T), (WholePlan<LOGN, k
       const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
       uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-      for (int j = 0; j < P::E; ++j)
-        __builtin_nontemporal_store(sub_lazy_mul_shoup(__builtin_nontemporal_load(&sl[j << 6]), v[j], qi, qis, q),
-                                    &dl[j << 6]);
+      for (int j = 0; j < P::E; ++j) {
+        if constexpr (kSplit) dl[j << 6] = sub_lazy_mul_shoup(sl[j << 6], v[j], qi, qis, q);
+        else __builtin_nontemporal_store(sub_lazy_mul_shoup(__builtin_nontemporal_load(&sl[j << 6]), v[j], qi, qis, q),
+                                         &dl[j << 6]);
+      }
     } else {
 #pragma unroll
       for (int j = 0; j < P::E; ++j) {
