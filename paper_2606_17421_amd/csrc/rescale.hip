@@ -13,7 +13,8 @@
 // decode-size layer), each workgroup instead takes one output limb of one
 // polynomial (kSplit): the inverse transform is repeated per limb, but the
 // chain per workgroup is two transforms instead of limbs, on limbs - 1 times
-// the workgroups, and with the latency plan (more lanes per transform).
+// the workgroups, and with the latency plan (more lanes per transform).  Rows
+// are read and written in the wave-coalesced layout.
 // N = 2^16: three passes through a workspace (see below).
 #include "ntt_core.hpp"
 
@@ -34,27 +35,20 @@ __global__ __launch_bounds__((WholePlan<LOGN, kSplit>::P::T), (WholePlan<LOGN, k
   const uint32_t top = limbs - 1;
   const uint32_t qt = tb.q[top];
 
-  // Up to 2^14 the rows are read and written in the wave-coalesced layout
-  // (re-laid out through each wave's LDS region), non-temporally when one
-  // workgroup takes a whole polynomial (each row is touched once).  The split
-  // route re-reads the top row in every limb's workgroup and keeps all its
-  // accesses cached (non-temporal there: 12.3 -> 13.3-13.8 us for 32
-  // ciphertexts at 2^13, 4 limbs).  At 2^15 the extra live registers of the
-  // coalesced path cost more than the coalescing gains, and there a wave's
-  // load or store of one element index covers 64 different cache lines, which
-  // the following indices reuse: those accesses must stay cached
-  // (non-temporal: 3.7 -> 6.3 ms at 3072 ciphertexts of 6 limbs).
-  constexpr bool kCoalesce = LOGN <= 14;
+  // The rows are read and written in the wave-coalesced layout (re-laid out
+  // through each wave's LDS region), non-temporally when one workgroup takes a
+  // whole polynomial (each row is touched once).  The split route re-reads the
+  // top row in every limb's workgroup and keeps all its accesses cached
+  // (non-temporal there: 12.3 -> 13.3-13.8 us for 32 ciphertexts at 2^13, 4
+  // limbs).  At 2^15 the coalesced path spills a few registers and still wins:
+  // 3.66-3.70 -> 3.33 ms for 3072 ciphertexts of 6 limbs, 147.5 -> 129.4 us
+  // for 64 (split), against loads and stores in the last group's layout, where
+  // a wave's access to one element index spans 64 cache lines.
   uint32_t v[P::E];
-  if constexpr (kCoalesce) {
-    const uint32_t* stop = src + static_cast<size_t>(top) * N + pos_coalesced<LOGE>(t, 0);
+  const uint32_t* stop = src + static_cast<size_t>(top) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-    for (int j = 0; j < P::E; ++j) v[j] = kSplit ? stop[j << 6] : __builtin_nontemporal_load(&stop[j << 6]);
-    wave_relayout<LOGN, LOGE, true>(v, t, lds);
-  } else {
-#pragma unroll
-    for (int j = 0; j < P::E; ++j) v[j] = src[static_cast<size_t>(top) * N + P::template pos<P::NG - 1>(t, j)];
-  }
+  for (int j = 0; j < P::E; ++j) v[j] = kSplit ? stop[j << 6] : __builtin_nontemporal_load(&stop[j << 6]);
+  wave_relayout<LOGN, LOGE, true>(v, t, lds);
   const size_t ttop = static_cast<size_t>(top) << LOGN;
   inv_block<LOGN, LOGN, LOGE>(v, t, 0, tb.inv + ttop, tb.inv_shoup + ttop, qt, lds);
   const uint32_t ni = tb.ninv[top], nis = tb.ninv_shoup[top];
@@ -73,22 +67,14 @@ __global__ __launch_bounds__((WholePlan<LOGN, kSplit>::P::T), (WholePlan<LOGN, k
     const size_t tl = static_cast<size_t>(l) << LOGN;
     fwd_block<LOGN, LOGN, LOGE, 0, false>(v, t, 0, tb.fwd + tl, tb.fwd_shoup + tl, q, lds);  // [0, 4q)
     const uint32_t qi = tb.qinv[top * tb.L + l], qis = tb.qinv_shoup[top * tb.L + l];
-    if constexpr (kCoalesce) {
-      wave_relayout<LOGN, LOGE, false>(v, t, lds);
-      const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
-      uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
+    wave_relayout<LOGN, LOGE, false>(v, t, lds);
+    const uint32_t* sl = src + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
+    uint32_t* dl = dst + static_cast<size_t>(l) * N + pos_coalesced<LOGE>(t, 0);
 #pragma unroll
-      for (int j = 0; j < P::E; ++j) {
-        if constexpr (kSplit) dl[j << 6] = sub_lazy_mul_shoup(sl[j << 6], v[j], qi, qis, q);
-        else __builtin_nontemporal_store(sub_lazy_mul_shoup(__builtin_nontemporal_load(&sl[j << 6]), v[j], qi, qis, q),
-                                         &dl[j << 6]);
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < P::E; ++j) {
-        const size_t x = static_cast<size_t>(l) * N + P::template pos<P::NG - 1>(t, j);
-        dst[x] = sub_lazy_mul_shoup(src[x], v[j], qi, qis, q);
-      }
+    for (int j = 0; j < P::E; ++j) {
+      if constexpr (kSplit) dl[j << 6] = sub_lazy_mul_shoup(sl[j << 6], v[j], qi, qis, q);
+      else __builtin_nontemporal_store(sub_lazy_mul_shoup(__builtin_nontemporal_load(&sl[j << 6]), v[j], qi, qis, q),
+                                       &dl[j << 6]);
     }
   }
 }
