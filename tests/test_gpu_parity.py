@@ -326,6 +326,43 @@ def test_encode_poly_large_coefficients(gpu_lib, log_n, limbs):
     print(f"encode_poly large N=2^{log_n}: {rows_equal} of {2 * limbs} limb rows identical")
 
 
+def test_encode_poly_mixed_batch_wide_vectors(gpu_lib):
+    """A batch with a few slot vectors whose coefficients pass 2^31 (offset by 4.0
+    at scale 2^30) among CKKS-scaled ones: each workgroup takes its own vector's
+    path.  The wide vectors match the oracle within the decoded-slot bound and
+    their own encoding alone; every other vector is bit-identical to a batch
+    without wide neighbours; no output word lies outside [0, q)."""
+    ck = gpu_lib
+    log_n, limbs, count = 10, 2, 600
+    ctx = ctx_for(ck, log_n, 3)
+    qs, psis, n = ctx.moduli[:limbs], ctx.roots[:limbs], 1 << log_n
+    delta = 2.0 ** 30
+    z = gen.poly_weights(np.random.default_rng(1010), 1, count, n // 2)[0]
+    wide = [0, 1, 255, 256, 511, count - 1]
+    z_mixed = z.copy()
+    z_mixed[wide] += 4.0
+    pt = ck.empty_u32((count, limbs, n))
+    ck.ckks_linear_encode_poly(ctx, ck.to_device(z_mixed), count, limbs, delta, pt)
+    got = ck.to_host_u32(pt)
+    pt_plain = ck.empty_u32((count, limbs, n))
+    ck.ckks_linear_encode_poly(ctx, ck.to_device(z), count, limbs, delta, pt_plain)
+    plain = ck.to_host_u32(pt_plain)
+    assert np.all(got.astype(np.uint64) < np.array(qs, dtype=np.uint64)[None, :, None]), "a word outside [0, q)"
+    others = np.setdiff1d(np.arange(count), wide)
+    assert np.array_equal(got[others], plain[others]), "a fitting vector changed beside wide ones"
+    one = ck.empty_u32((1, limbs, n))
+    for v in wide:
+        ck.ckks_linear_encode_poly(ctx, ck.to_device(z_mixed[v:v + 1]), 1, limbs, delta, one)
+        assert np.array_equal(got[v], ck.to_host_u32(one)[0]), f"wide vector {v} differs from its own encoding"
+    for v in (wide[0], wide[3], wide[-1]):
+        want = OE.encode_poly(z_mixed[v:v + 1], delta, qs, psis, log_n).astype(np.uint32)
+        assert np.max(np.abs(OE.round_coeffs(OE.encode_coeffs(z_mixed[v:v + 1], log_n), delta))) >= 2 ** 31
+        sl_got = _decode_rows(got[v:v + 1], qs, psis, log_n, delta)
+        sl_want = _decode_rows(want, qs, psis, log_n, delta)
+        err = np.max(np.abs(sl_got - sl_want))
+        assert err <= 2.0 ** -20 * max(1.0, np.max(np.abs(sl_want))), (v, err)
+
+
 def test_tiny_layer_end_to_end(gpu_lib):
     """Tiny encrypted layer: GPU encode + MAC + rescale bit-exact, then decrypts to W.x."""
     ck = gpu_lib
